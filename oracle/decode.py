@@ -1,0 +1,112 @@
+"""Oracle of the RPS decoding loop (Algorithm 1, Appendix A).
+
+``forward(batch_tokens, m_pos)`` is any model: it returns, for every sequence
+of the batch, (Stats over rows m_pos, log p of requested tokens at rows).
+The loop itself only follows Algorithm 1:
+
+  for each block b (left to right):
+      block-opening forward; M <- masked positions of block b
+      while M is not empty:
+          standard (confidence-aware) commit of S, fallback to the most
+          confident position; M <- M minus S; stop the block if M is empty
+          pivot selection (Eq. 3); if infeasible: normal forward, continue
+          candidate set; if at most one real candidate: normal forward, continue
+          lookahead forward over [anchor, branch_1, ..., branch_n]
+          Eq. 4 decision; commit c* at i* and carry the winner's
+          distributions, or abstain and carry the anchor's
+
+Every forward is counted (NFE), split into normal and lookahead passes as in
+the paper's speedup decomposition (Table 4).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from . import rps
+
+
+@dataclass
+class DecodeResult:
+    tokens: np.ndarray
+    nfe: int = 0
+    normal: int = 0
+    lookahead: int = 0
+    commits_conf: int = 0
+    commits_pivot: int = 0
+    abstains: int = 0
+    trace: list = field(default_factory=list)
+
+
+def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps.Params,
+               lam: float, tau: float, capacity: int = 16, max_iters: int = 100000) -> DecodeResult:
+    prompt = np.asarray(prompt, dtype=np.int64)
+    P = len(prompt)
+    tokens = np.concatenate([prompt, np.full(gen_len, mask_id, dtype=np.int64)])
+    res = DecodeResult(tokens=tokens)
+    iters = 0
+    for b in range(gen_len // block):
+        m_pos = np.arange(P + b * block, P + (b + 1) * block)
+        m_pos = m_pos[tokens[m_pos] == mask_id]
+        stats = forward(tokens[None, :], m_pos, None)[0][0]
+        res.nfe += 1
+        res.normal += 1
+        state = rps.State(tokens, m_pos, stats)
+        while len(state.m_pos) > 0:
+            iters += 1
+            assert iters <= max_iters
+            committed, _ = rps.apply_confidence_commit(state, tau, mask_id)
+            res.commits_conf += len(committed)
+            res.trace.append(("commit", [int(c) for c in committed]))
+            if len(state.m_pos) == 0:
+                break
+            plan = rps.select_pivots(state.stats, state.m_pos, prm)
+            plan.pivots = plan.pivots[:1]
+            brs = plan.branches()[:capacity - 1]
+            if not brs:
+                state.stats = forward(state.tokens[None, :], state.m_pos, None)[0][0]
+                res.nfe += 1
+                res.normal += 1
+                res.trace.append(("skip",))
+                continue
+            pv = plan.pivots[0]
+            pv.tokens, pv.logp = pv.tokens[:len(brs)], pv.logp[:len(brs)]
+            batch = rps.branch_tokens(state.tokens, plan, with_anchor=True)
+            probe = [(pv.row, t) for t in pv.tokens]
+            outs = forward(batch, state.m_pos, probe)
+            res.nfe += 1
+            res.lookahead += 1
+            anchor, anchor_probe = outs[0]
+            branch_stats = [o[0] for o in outs[1:]]
+            dec = rps.score(anchor, branch_stats, plan, lam, anchor_logp=anchor_probe)
+            res.trace.append(("lookahead", pv.pos, dec.token if dec.commit else -1))
+            if dec.commit:
+                res.commits_pivot += 1
+            else:
+                res.abstains += 1
+            rps.apply_decision(state, dec, branch_stats, anchor)
+        tokens = state.tokens
+    res.tokens = tokens
+    return res
+
+
+def model_forward(weights, shape, topk: int = 16, scales=None, scale: float = 1.0,
+                  mirror: bool = False):
+    """Forward callback for ``rps_decode`` backed by the oracle transformer.
+
+    scales: optional per-absolute-position logit scale array (indexed by position).
+    """
+    from .model import forward_logits
+    from .stats import softmax_stats
+
+    def fwd(batch, m_pos, probe):
+        rs = None if scales is None else np.asarray(scales)[np.asarray(m_pos)]
+        logits = forward_logits(batch, weights, shape, m_pos, mirror=mirror, row_scale=rs, scale=scale)
+        out = []
+        for b in range(logits.shape[0]):
+            st = softmax_stats(logits[b], topk)
+            pl = None if probe is None else [float(logits[b][row, tok] - st.lse[row]) for row, tok in probe]
+            out.append((st, pl))
+        return out
+    return fwd

@@ -1,0 +1,158 @@
+"""Oracle forward pass of the masked-diffusion transformer, float64.
+
+The paper treats the dLLM as a black box that returns p_i = p_theta(. | y, x)
+for every masked position in one forward pass over [y || x] (Section 3,
+Notation).  The architecture used here is a LLaMA-style bidirectional
+transformer: pre-RMSNorm (unit gain), rotate-half RoPE, full non-causal
+softmax attention, SwiGLU feed-forward, untied embedding and LM head, no biases.
+
+Every operation is its textbook definition written out once; matrix products
+use numpy's matmul in float64.
+
+``mirror=True`` rounds values to bfloat16 (nearest-even) at the points where
+the GPU contract stores bfloat16: the inputs of every projection (normed
+activations, attention output, SwiGLU output), Q/K/V after RoPE and the final
+normed hidden state.  Everything else stays float64.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to the nearest bfloat16 value (ties to even), kept as float64."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    b = x.view(np.uint64)
+    drop = np.uint64(45)                      # float64 keeps 52 mantissa bits, bfloat16 keeps 7
+    half = np.uint64((1 << 44) - 1)
+    lsb = (b >> drop) & np.uint64(1)
+    with np.errstate(over="ignore"):
+        r = ((b + half + lsb) >> drop) << drop
+    return r.view(np.float64)
+
+
+def rmsnorm(x: np.ndarray, eps: float) -> np.ndarray:
+    """x / sqrt(mean(x^2) + eps) over the last axis (gain 1)."""
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps)
+
+
+def rope(u: np.ndarray, pos: np.ndarray, base: float) -> np.ndarray:
+    """Rotate-half rotary embedding.
+
+    u: [..., S, hd]; pos: [S] absolute position ids.  For j < hd/2 the pair
+    (u_j, u_{j+hd/2}) is rotated by the angle pos * base^(-2j/hd).
+    """
+    hd = u.shape[-1]
+    half = hd // 2
+    theta = base ** (-2.0 * np.arange(half, dtype=np.float64) / hd)
+    ang = pos.astype(np.float64)[:, None] * theta[None, :]
+    c, s = np.cos(ang), np.sin(ang)
+    u1, u2 = u[..., :half], u[..., half:]
+    return np.concatenate([u1 * c - u2 * s, u1 * s + u2 * c], axis=-1)
+
+
+def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
+    """Non-causal softmax attention: softmax(q k^T / sqrt(hd)) v over all keys.
+
+    q: [H, Sq, hd], k, v: [H, Sk, hd] -> [H, Sq, hd].
+    """
+    hd = q.shape[-1]
+    s = q @ np.swapaxes(k, -1, -2) / np.sqrt(hd)
+    s = s - s.max(axis=-1, keepdims=True)
+    p = np.exp(s)
+    p = p / p.sum(axis=-1, keepdims=True)
+    return p @ v
+
+
+def silu(x: np.ndarray) -> np.ndarray:
+    return x / (1.0 + np.exp(-x))
+
+
+def _w(weights, name) -> np.ndarray:
+    return np.asarray(weights[name], dtype=np.float64)
+
+
+def layer(x, weights, l, shape, pos, mirror=False, prefix_kv=None, collect=None):
+    """One transformer layer on one sequence.
+
+    x: [S, d] residual stream.  prefix_kv: optional (k, v) of a cached prefix,
+    each [H, P, hd] (post-RoPE); the S block positions then attend to the
+    prefix keys followed by their own keys.  collect: optional list that
+    receives this layer's (k, v), each [H, S, hd].
+    """
+    R = bf16_round if mirror else (lambda t: t)
+    S, d = x.shape
+    H, hd = shape.n_heads, shape.head_dim
+    a = R(rmsnorm(x, shape.rms_eps))
+    qkv = a @ _w(weights, f"layers.{l}.wqkv").T                   # [S, 3d]
+    q = qkv[:, 0 * d:1 * d].reshape(S, H, hd).transpose(1, 0, 2)  # [H, S, hd]
+    k = qkv[:, 1 * d:2 * d].reshape(S, H, hd).transpose(1, 0, 2)
+    v = qkv[:, 2 * d:3 * d].reshape(S, H, hd).transpose(1, 0, 2)
+    q = R(rope(q, pos, shape.rope_base))
+    k = R(rope(k, pos, shape.rope_base))
+    v = R(v)
+    if collect is not None:
+        collect.append((k, v))
+    if prefix_kv is not None:
+        kk = np.concatenate([prefix_kv[0], k], axis=1)
+        vv = np.concatenate([prefix_kv[1], v], axis=1)
+    else:
+        kk, vv = k, v
+    o = attention(q, kk, vv).transpose(1, 0, 2).reshape(S, d)
+    o = R(o)
+    x = x + o @ _w(weights, f"layers.{l}.wo").T
+    b = R(rmsnorm(x, shape.rms_eps))
+    gu = b @ _w(weights, f"layers.{l}.wgu").T                     # [S, 2F]
+    F = shape.d_ffn
+    f = R(silu(gu[:, :F]) * gu[:, F:])
+    return x + f @ _w(weights, f"layers.{l}.wdown").T
+
+
+def hidden(tokens, weights, shape, pos_offset=0, mirror=False, prefix_kv=None, collect=None):
+    """Final normed hidden states of one sequence.
+
+    tokens: [S] int; positions are pos_offset + t.  prefix_kv: optional list
+    (one entry per layer) of cached (k, v).  collect: optional list that
+    receives per-layer (k, v).
+    """
+    tokens = np.asarray(tokens, dtype=np.int64)
+    pos = pos_offset + np.arange(tokens.shape[0])
+    x = _w(weights, "emb")[tokens]
+    for l in range(shape.n_layers):
+        x = layer(x, weights, l, shape, pos, mirror=mirror,
+                  prefix_kv=None if prefix_kv is None else prefix_kv[l], collect=collect)
+    h = rmsnorm(x, shape.rms_eps)
+    return bf16_round(h) if mirror else h
+
+
+def lm_logits(h, weights, shape, row_scale=None, scale=1.0):
+    """Scaled LM-head logits with the [MASK] logit removed (set to -inf).
+
+    h: [R, d].  logits = scale * row_scale_r * (h W_lm^T).
+    """
+    logits = h @ _w(weights, "lm_head").T
+    s = np.full(h.shape[0], float(scale)) if row_scale is None else float(scale) * np.asarray(row_scale, np.float64)
+    logits = logits * s[:, None]
+    logits[:, shape.mask_id] = -np.inf
+    return logits
+
+
+def forward_logits(tokens_batch, weights, shape, lm_pos, pos_offset=0, mirror=False,
+                   prefix_kv=None, row_scale=None, scale=1.0):
+    """Logits at positions lm_pos of every sequence in the batch.
+
+    tokens_batch: [B, S].  Returns [B, len(lm_pos), V] (float64).
+    row_scale: optional per-position scale, indexed like lm_pos.
+    """
+    out = []
+    for tokens in np.asarray(tokens_batch):
+        h = hidden(tokens, weights, shape, pos_offset=pos_offset, mirror=mirror, prefix_kv=prefix_kv)
+        out.append(lm_logits(h[np.asarray(lm_pos)], weights, shape, row_scale=row_scale, scale=scale))
+    return np.stack(out)
+
+
+def prefix_cache(tokens, weights, shape, mirror=False):
+    """Post-RoPE per-layer (k, v) of a prefix forward pass, each [H, P, hd]."""
+    kv = []
+    hidden(tokens, weights, shape, mirror=mirror, collect=kv)
+    return kv
