@@ -1,0 +1,214 @@
+"""Benchmark of the batched RPS denoising step on one MI355X.
+
+Default workload: the 8B-shape RPS lookahead step (bf16): 32 layers,
+d 4096, 32 x 128 heads, SwiGLU FFN 12288, vocabulary 126464, random weights;
+one sequence of 256 random prompt tokens + 256 masked positions.  A step
+selects 4 mid-entropy pivots (25th-75th entropy percentile band) x 4
+candidate tokens from the carried statistics, runs the 16 branch sequences
+of 512 tokens through the model with the fused LM-head statistics on the
+16 x 256 masked rows, scores them (Eq. 4, lambda 0) and commits.
+
+Prints one JSON line.  `value` is RPS steps per second with weights and
+state resident in HBM; `roofline` covers the dominant kernel (the gate/up
+projection GEMM), timed with HIP events on the launch stream during the
+timed steps; `cpu_baseline` times the CPU oracle on a bounded sample of the
+same work (2 of the 32 layers of one branch sequence and the LM head on 64
+of its masked rows), scaled to one step.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+from synth import workloads as W  # noqa: E402
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+METRIC = "denoising steps/sec and committed tokens/sec, 8B-shape, lookahead batch 16"
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def build_state(P, model, wl, dev):
+    shape = wl.model
+    prompt = synth.tokens_torch(W.SEED_PROMPT, "prompt", wl.prompt_len, shape.vocab - 1, device=dev)
+    tokens = torch.cat([prompt, torch.full((wl.gen_len,), shape.mask_id, dtype=torch.int32, device=dev)])
+    m_pos = torch.arange(wl.prompt_len, wl.seq, dtype=torch.int32, device=dev)
+    base = model.forward(tokens[None], m_pos, scale=wl.logit_scale, k=wl.topk)
+    return tokens, m_pos, base
+
+
+def linear_flops(shape, rows):
+    d, f = shape.d_model, shape.d_ffn
+    return {"gemm_qkv": 2.0 * rows * 3 * d * d, "gemm_o": 2.0 * rows * d * d,
+            "gemm_gateup": 2.0 * rows * 2 * f * d, "gemm_down": 2.0 * rows * f * d}
+
+
+def step_flops(shape, batch, seq, lm_rows):
+    per_layer = sum(linear_flops(shape, batch * seq).values()) + 4.0 * batch * seq * seq * shape.d_model
+    return shape.n_layers * per_layer + 2.0 * lm_rows * shape.d_model * shape.vocab
+
+
+def cpu_baseline(wl, w_dev, tokens_np, m_pos_np, n_layers_sample=2, lm_rows_sample=64):
+    """Oracle (float64 numpy, bf16 rounding at the GPU's storage points) on a bounded sample."""
+    from threadpoolctl import threadpool_info
+    from oracle import model as om
+    from oracle.stats import softmax_stats
+    shape = wl.model
+    wts = {"emb": w_dev["emb"][torch.from_numpy(tokens_np.astype(np.int64)).to(w_dev["emb"].device)].float().cpu().numpy()}
+    for l in range(n_layers_sample):
+        for n in synth.WEIGHT_NAMES:
+            wts[f"layers.{l}.{n}"] = w_dev[f"layers.{l}.{n}"].float().cpu().numpy()
+    wts["lm_head"] = w_dev["lm_head"].float().cpu().numpy()
+    S = tokens_np.shape[0]
+    pos = np.arange(S)
+    x = wts["emb"].astype(np.float64)            # rows already gathered for this sequence
+    t0 = time.perf_counter()
+    for l in range(n_layers_sample):
+        x = om.layer(x, wts, l, shape, pos, mirror=True)
+    t_layers = time.perf_counter() - t0
+    h = om.bf16_round(om.rmsnorm(x[m_pos_np[:lm_rows_sample]], shape.rms_eps))
+    t1 = time.perf_counter()
+    logits = om.lm_logits(h, wts, shape, scale=wl.logit_scale)
+    softmax_stats(logits, wl.topk)
+    t_lm = time.perf_counter() - t1
+    n_branch = wl.n_pivots * wl.n_cand
+    n_m = len(m_pos_np)
+    t_step = n_branch * (t_layers / n_layers_sample * shape.n_layers + t_lm / lm_rows_sample * n_m)
+    threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    return {"value": 1.0 / t_step, "unit": "steps/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"one 512-token branch sequence through {n_layers_sample} of {shape.n_layers} layers "
+                       f"({t_layers:.2f} s) and the LM head + statistics on {lm_rows_sample} of its {n_m} "
+                       f"masked rows ({t_lm:.2f} s), scaled x{n_branch} branches, x{shape.n_layers} layers, "
+                       f"x{n_m} rows to one step ({t_step:.1f} s)"),
+            "sample_seconds": round(t_layers + t_lm, 2), "host_cpus": os.cpu_count()}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="b8_rps_step_bf16", choices=["b8_rps_step_bf16"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layers", type=int, default=0, help="override layer count (profiling runs only)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the lookahead branches would shard "
+              "across GPUs by data parallelism, which this build does not implement.", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    import paper_2608_11742_amd as P
+
+    wl = W.WORKLOADS[args.workload]
+    if args.layers:
+        import dataclasses
+        wl = dataclasses.replace(wl, model=dataclasses.replace(wl.model, n_layers=args.layers))
+    shape = wl.model
+    dev = torch.device("cuda:0")
+    t = time.perf_counter()
+    w = synth.model_weights_torch(shape, seed=W.SEED_WEIGHTS, dtype="bf16", device=dev)
+    torch.cuda.synchronize()
+    log(f"weights generated on device in {time.perf_counter() - t:.1f} s "
+        f"({shape.n_params() / 1e9:.2f} B params)")
+    model = P.Model(shape, w, dtype="bf16", max_pos=wl.seq)
+    tokens, m_pos, base = build_state(P, model, wl, dev)
+    prm = P.params(mode=wl.pivot_mode, k_max=wl.k_max, tau_pivot=wl.tau_pivot, pct_lo=wl.pct_lo,
+                   pct_hi=wl.pct_hi, n_pivots=wl.n_pivots, r=wl.r, n_cand=wl.n_cand, max_branch=wl.capacity)
+    snap = (tokens.clone(), m_pos.clone(), base.numpy())
+
+    def fresh_step():
+        tokens.copy_(snap[0])
+        m_pos.copy_(snap[1])
+        for k, v in snap[2].items():
+            getattr(base, k).copy_(torch.from_numpy(v))
+        return P.RpsStep(model, tokens, m_pos, base, prm, lam=wl.lam, capacity=wl.capacity,
+                         scale=wl.logit_scale)
+
+    stp = fresh_step()
+    for i in range(args.warmup):
+        stp.run()
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} steps done")
+
+    stp = fresh_step()
+    n0 = stp.n_m
+    P.dllm_profile_begin(model.handle, 400 * (args.steps + 1))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        stp.run()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = P.dllm_profile_end(model.handle)
+    committed = n0 - stp.n_m
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    log(f"timed {args.steps} steps: {ms_per_step:.2f} ms/step, committed {committed}")
+
+    rows = wl.capacity * wl.seq
+    lf = linear_flops(shape, rows)
+    kern = {}
+    for name, (ms, n) in prof.items():
+        if n:
+            kern[name] = {"ms_per_launch": round(ms / n, 4), "launches": n, "ms_total": round(ms, 3)}
+    for name in lf:
+        if name in kern:
+            kern[name]["tflops"] = round(lf[name] / (kern[name]["ms_per_launch"] * 1e-3) / 1e12, 1)
+    dom = "gemm_gateup"
+    achieved = lf[dom] / (kern[dom]["ms_per_launch"] * 1e-3) / 1e12
+    total_flops = step_flops(shape, wl.capacity, wl.seq, wl.capacity * n0)
+    res = {
+        "metric": METRIC,
+        "value": round(1e3 / ms_per_step, 4),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded random weights and prompt tokens)",
+        "config": {
+            "workload": (f"8B-shape RPS lookahead step: {shape.n_layers} layers, d {shape.d_model}, "
+                         f"{shape.n_heads}x{shape.head_dim} heads, FFN {shape.d_ffn}, vocab {shape.vocab}; "
+                         f"{wl.n_pivots} pivots x {wl.n_cand} candidates = {wl.capacity} sequences of "
+                         f"{wl.seq} ({wl.prompt_len} prompt + {wl.gen_len} masked); stats on the masked rows"),
+            "batch": wl.capacity, "seq_len": wl.seq, "lm_rows": wl.capacity * n0,
+        },
+        "committed_tokens_per_s": round(committed / (t1 - t0), 3),
+        "step_tflop": round(total_flops / 1e12, 2),
+        "step_tflops_achieved": round(total_flops / (ms_per_step * 1e-3) / 1e12, 1),
+        "roofline": {
+            "bound": "mfma", "kernel": "gemm_gateup (gate/up projection + SwiGLU epilogue)",
+            "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "flop_per_launch": lf[dom],
+        },
+        "kernels": kern,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle sample")
+        res["cpu_baseline"] = cpu_baseline(wl, w, snap[0].cpu().numpy(), snap[1].cpu().numpy())
+        log("CPU sample done")
+    model.close()
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

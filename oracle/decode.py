@@ -41,6 +41,8 @@ class DecodeResult:
 
 def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps.Params,
                lam: float, tau: float, capacity: int = 16, max_iters: int = 100000) -> DecodeResult:
+    import dataclasses
+    prm = dataclasses.replace(prm, max_branch=min(prm.max_branch, capacity - 1))   # slot 0: anchor
     prompt = np.asarray(prompt, dtype=np.int64)
     P = len(prompt)
     tokens = np.concatenate([prompt, np.full(gen_len, mask_id, dtype=np.int64)])
@@ -63,7 +65,7 @@ def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps
                 break
             plan = rps.select_pivots(state.stats, state.m_pos, prm)
             plan.pivots = plan.pivots[:1]
-            brs = plan.branches()[:capacity - 1]
+            brs = plan.branches()
             if not brs:
                 state.stats = forward(state.tokens[None, :], state.m_pos, None)[0][0]
                 res.nfe += 1
@@ -71,7 +73,6 @@ def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps
                 res.trace.append(("skip",))
                 continue
             pv = plan.pivots[0]
-            pv.tokens, pv.logp = pv.tokens[:len(brs)], pv.logp[:len(brs)]
             batch = rps.branch_tokens(state.tokens, plan, with_anchor=True)
             probe = [(pv.row, t) for t in pv.tokens]
             outs = forward(batch, state.m_pos, probe)

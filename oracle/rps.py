@@ -40,6 +40,7 @@ class Params:
     n_pivots: int = 1
     r: float = 0.1
     n_cand: int = 10
+    max_branch: int = 16      # lookahead capacity: branches beyond it are dropped
 
 
 @dataclass
@@ -119,6 +120,8 @@ def select_pivots(st: Stats, m_pos, prm: Params) -> Plan:
 
     Returns an empty plan when no pivot is feasible or when the chosen
     pivot has at most one real candidate (both skip rules of Algorithm 1).
+    Candidates beyond the lookahead capacity (max_branch branches in total)
+    are dropped before that check.
     """
     m_pos = np.asarray(m_pos)
     n = len(m_pos)
@@ -142,6 +145,7 @@ def select_pivots(st: Stats, m_pos, prm: Params) -> Plan:
     order = cand_rows[np.lexsort((m_pos[cand_rows], -htr[cand_rows]))]
     chosen = order[:prm.n_pivots]
     plan = Plan()
+    used = 0
     for rank, j in enumerate(chosen):
         nxt = [htr[order[rank + 1]]] if rank + 1 < len(order) else []
         prv = [htr[order[rank - 1]]] if rank > 0 else []
@@ -152,6 +156,7 @@ def select_pivots(st: Stats, m_pos, prm: Params) -> Plan:
         pmax = math.exp(st.lmax[j] - st.lse[j])
         ratio = p / pmax
         keep = [k for k in range(len(p)) if ratio[k] >= prm.r][:prm.n_cand]
+        keep = keep[:max(0, prm.max_branch - used)]
         cand_margin = float(np.min(np.abs(ratio - prm.r))) if prm.r > 0 else math.inf
         pv = Pivot(row=int(j), pos=int(m_pos[j]),
                    tokens=[int(st.topk_id[j, k]) for k in keep],
@@ -160,6 +165,7 @@ def select_pivots(st: Stats, m_pos, prm: Params) -> Plan:
                    cand_margin=cand_margin)
         if len(pv.tokens) > 1:
             plan.pivots.append(pv)
+            used += len(pv.tokens)
     return plan
 
 

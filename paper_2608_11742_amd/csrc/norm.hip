@@ -1,0 +1,102 @@
+// Row-wise kernels of the forward: embedding gather, RMSNorm (optionally
+// gathering rows) and the prefix-cache writer.
+#include "kernels.h"
+#include "common.h"
+
+namespace dllm {
+
+namespace {
+
+constexpr int kRowThreads = 256;
+
+template <typename T>
+__global__ __launch_bounds__(kRowThreads) void embed_kernel(const int32_t* __restrict__ tok, const T* __restrict__ emb,
+                                                            int d, int vocab, float* __restrict__ x) {
+  const int r = blockIdx.x;
+  const int t = min(max(tok[r], 0), vocab - 1);
+  const T* src = emb + size_t(t) * d;
+  float* dst = x + size_t(r) * d;
+  for (int c = threadIdx.x; c < d; c += kRowThreads) dst[c] = load_f(src + c);
+}
+
+// One workgroup per output row; the sum of squares is reduced in fp32 over
+// 4 waves.
+template <typename T>
+__global__ __launch_bounds__(kRowThreads) void rmsnorm_kernel(const float* __restrict__ x, int d, float eps,
+                                                              const int32_t* __restrict__ pos, int n_pos, int seq,
+                                                              T* __restrict__ out) {
+  __shared__ float part[kRowThreads / kWave];
+  const int r = blockIdx.x;
+  const int src_row = pos ? (r / n_pos) * seq + min(max(pos[r % n_pos], 0), seq - 1) : r;
+  const float* xr = x + size_t(src_row) * d;
+  float ss = 0.f;
+  for (int c = threadIdx.x * 4; c < d; c += kRowThreads * 4) {
+    const float4 v = *reinterpret_cast<const float4*>(xr + c);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < kRowThreads / kWave; ++w) tot += part[w];
+  const float inv = 1.0f / sqrtf(tot / float(d) + eps);
+  T* o = out + size_t(r) * d;
+  for (int c = threadIdx.x * 4; c < d; c += kRowThreads * 4) {
+    const float4 v = *reinterpret_cast<const float4*>(xr + c);
+    store_f(o + c + 0, v.x * inv);
+    store_f(o + c + 1, v.y * inv);
+    store_f(o + c + 2, v.z * inv);
+    store_f(o + c + 3, v.w * inv);
+  }
+}
+
+// grid: (H, rows of this call); copies K rows and V^T columns into the cache
+template <typename T>
+__global__ __launch_bounds__(kRowThreads) void kv_store_kernel(const T* __restrict__ k, const T* __restrict__ vt,
+                                                               int seq, int hd, int vt_ld, T* __restrict__ ck,
+                                                               T* __restrict__ cvt, int cap, int off) {
+  const int h = blockIdx.x, s = blockIdx.y;
+  for (int c = threadIdx.x; c < hd; c += kRowThreads) {
+    ck[(size_t(h) * cap + off + s) * hd + c] = k[(size_t(h) * seq + s) * hd + c];
+    cvt[(size_t(h) * hd + c) * cap + off + s] = vt[(size_t(h) * hd + c) * vt_ld + s];
+  }
+}
+
+}  // namespace
+
+hipError_t embed(int dtype, const int32_t* tok, int rows, const void* emb, int d, int vocab, float* x, hipStream_t s) {
+  if (dtype)
+    hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(rows), dim3(kRowThreads), 0, s, tok,
+                       static_cast<const bf16_t*>(emb), d, vocab, x);
+  else
+    hipLaunchKernelGGL(embed_kernel<float>, dim3(rows), dim3(kRowThreads), 0, s, tok,
+                       static_cast<const float*>(emb), d, vocab, x);
+  return hipGetLastError();
+}
+
+hipError_t rmsnorm(int dtype, const float* x, int d, float eps, int rows, const int32_t* pos, int n_pos, int seq,
+                   void* out, hipStream_t s) {
+  if (dtype)
+    hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(rows), dim3(kRowThreads), 0, s, x, d, eps, pos, n_pos, seq,
+                       static_cast<bf16_t*>(out));
+  else
+    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(rows), dim3(kRowThreads), 0, s, x, d, eps, pos, n_pos, seq,
+                       static_cast<float*>(out));
+  return hipGetLastError();
+}
+
+hipError_t kv_store(int dtype, const void* k, const void* vt, int H, int seq, int hd, int vt_ld, void* ck,
+                    void* cvt, int cap, int off, hipStream_t s) {
+  if (dtype)
+    hipLaunchKernelGGL(kv_store_kernel<bf16_t>, dim3(H, seq), dim3(kRowThreads), 0, s,
+                       static_cast<const bf16_t*>(k), static_cast<const bf16_t*>(vt), seq, hd, vt_ld,
+                       static_cast<bf16_t*>(ck), static_cast<bf16_t*>(cvt), cap, off);
+  else
+    hipLaunchKernelGGL(kv_store_kernel<float>, dim3(H, seq), dim3(kRowThreads), 0, s,
+                       static_cast<const float*>(k), static_cast<const float*>(vt), seq, hd, vt_ld,
+                       static_cast<float*>(ck), static_cast<float*>(cvt), cap, off);
+  return hipGetLastError();
+}
+
+}  // namespace dllm

@@ -1,0 +1,159 @@
+"""GPU parity at the 8B-class shapes, in the launch configuration the benchmark
+times (16 sequences x 512 tokens, LM head on 16 x 256 rows), checked on
+sampled outputs the oracle can compute, and by properties that hold at any size."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from synth import workloads as W
+from oracle import model as om
+from oracle import rps as orps
+from oracle.stats import softmax_stats
+from tests.parity import compare_stats, MARGIN
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+B8 = synth.B8
+
+
+@pytest.fixture(scope="module")
+def P():
+    import paper_2608_11742_amd as P
+    return P
+
+
+@pytest.fixture(scope="module")
+def lm_head():
+    return synth.weight_torch(W.SEED_WEIGHTS, "lm_head", (B8.vocab, B8.d_model), dtype="bf16", device=DEV)
+
+
+@pytest.mark.parametrize("R", [4096, 4000])
+def test_lm_head_stats_full_shape_sampled_rows(P, lm_head, R):
+    """vocab_entropy_topk at the step's LM-head shape; 24 sampled rows against the oracle."""
+    h = synth.weight_torch(21, "hidden", (R, B8.d_model), std=1.0, dtype="bf16", device=DEV)
+    rs = torch.from_numpy((0.5 + 3 * synth.uniform01_np(22, "rs", R)).astype(np.float32)).to(DEV)
+    out = P.Stats(R, 16, device=DEV)
+    ws = torch.empty(P.vocab_entropy_topk_workspace_bytes(R, B8.vocab), dtype=torch.uint8, device=DEV)
+    P.vocab_entropy_topk(h, lm_head, out, ws, row_scale=rs, scale=1.0, mask_id=B8.mask_id)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, 1, 127, 128, R - 1], synth.tokens_np(23, "rows", 19, R)]))
+    hn = h[torch.from_numpy(rows).to(DEV)].float().cpu().numpy().astype(np.float64)
+    wn = lm_head.float().cpu().numpy().astype(np.float64)
+    logits = rs.cpu().numpy()[rows].astype(np.float64)[:, None] * (hn @ wn.T)
+    logits[:, B8.mask_id] = -np.inf
+    ref = softmax_stats(logits, 16)
+    got = {k: v[rows] for k, v in out.numpy().items()}
+    print(compare_stats(got, ref, 1e-3, label=f"lm head R={R}"))
+
+
+@pytest.fixture(scope="module")
+def b8_two_layer(P, lm_head):
+    shape = dataclasses.replace(B8, n_layers=2)
+    w = synth.model_weights_torch(shape, seed=W.SEED_WEIGHTS, dtype="bf16", device=DEV, layers=range(2))
+    m = P.Model(shape, w, dtype="bf16", max_pos=512)
+    yield shape, w, m
+    m.close()
+
+
+def _branch_batch(shape, n_branch=16, P_=256, G=256):
+    prompt = synth.tokens_np(W.SEED_PROMPT, "prompt", P_, shape.vocab - 1)
+    toks = np.concatenate([prompt, np.full(G, shape.mask_id, np.int32)])
+    batch = np.repeat(toks[None], n_branch, axis=0)
+    piv = P_ + synth.tokens_np(31, "piv", n_branch, G)
+    cand = synth.tokens_np(32, "cand", n_branch, shape.vocab - 1)
+    batch[np.arange(n_branch), piv] = cand
+    return batch, np.arange(P_, P_ + G, dtype=np.int32)
+
+
+def test_two_layer_8b_width_forward_in_bench_launch_config(P, b8_two_layer):
+    """16 x 512 batch (M = 8192 GEMM rows) through 2 layers of 8B width; sequence 5
+    against the mirror oracle on 32 sampled masked rows."""
+    shape, w, model = b8_two_layer
+    batch, m_pos = _branch_batch(shape)
+    out = model.forward(torch.from_numpy(batch).to(DEV), torch.from_numpy(m_pos).to(DEV), scale=4.0)
+    torch.cuda.synchronize()
+    b = 5
+    w_np = {k: v.float().cpu().numpy() for k, v in w.items()}
+    sample = np.unique(np.concatenate([[0, 255], synth.tokens_np(33, "s", 30, 256)]))
+    h = om.hidden(batch[b], w_np, shape, mirror=True)[m_pos[sample]]
+    ref = softmax_stats(om.lm_logits(h, w_np, shape, scale=4.0), 16)
+    got = {k: v[b * 256 + sample] for k, v in out.numpy().items()}
+    print(compare_stats(got, ref, 2e-2, label="2-layer 8B width"))
+
+
+def test_batch_invariance(P, b8_two_layer):
+    """A branch's statistics do not depend on the other sequences of its batch."""
+    shape, w, model = b8_two_layer
+    batch, m_pos = _branch_batch(shape)
+    m_dev = torch.from_numpy(m_pos).to(DEV)
+    full = model.forward(torch.from_numpy(batch).to(DEV), m_dev).numpy()
+    for b in (0, 9):
+        one = model.forward(torch.from_numpy(batch[b:b + 1]).to(DEV), m_dev).numpy()
+        sl = slice(b * 256, (b + 1) * 256)
+        for k in ("H", "lse", "lmax", "topk_logit"):
+            assert np.max(np.abs(full[k][sl] - one[k])) < 1e-5, k
+        assert np.array_equal(full["argmax"][sl], one["argmax"])
+
+
+@pytest.fixture(scope="module")
+def b8_full(P):
+    w = synth.model_weights_torch(B8, seed=W.SEED_WEIGHTS, dtype="bf16", device=DEV)
+    m = P.Model(B8, w, dtype="bf16", max_pos=512)
+    yield w, m
+    m.close()
+
+
+def test_full_step_properties(P, b8_full):
+    """One 32-layer RPS lookahead step (the benchmark's workload): plan, branches,
+    decision and commit are consistent with their definitions."""
+    w, model = b8_full
+    wl = W.WORKLOADS["b8_rps_step_bf16"]
+    prompt = synth.tokens_torch(W.SEED_PROMPT, "prompt", wl.prompt_len, B8.vocab - 1, device=DEV)
+    tokens = torch.cat([prompt, torch.full((wl.gen_len,), B8.mask_id, dtype=torch.int32, device=DEV)])
+    m_pos = torch.arange(wl.prompt_len, wl.seq, dtype=torch.int32, device=DEV)
+    base = model.forward(tokens[None], m_pos)
+    b0 = base.numpy()
+    t0 = tokens.cpu().numpy()
+    prm = P.params(mode="band", k_max=10, n_pivots=4, r=0.0, n_cand=4, max_branch=16)
+    stp = P.RpsStep(model, tokens, m_pos, base, prm, lam=0.0, capacity=16)
+    stp.run()
+    torch.cuda.synchronize()
+    plan = P.read_plan(stp.plan)
+    assert plan.n_pivots == 4 and plan.n_branch == 16
+    # pivots lie in the entropy band and are the feasible rows of largest truncated entropy
+    H = b0["H"].astype(np.float64)
+    lo, hi = np.percentile(H, 25), np.percentile(H, 75)
+    lp = b0["topk_logit"][:, :10].astype(np.float64) - b0["lse"][:, None]
+    htr = -(np.exp(lp) * lp).sum(1)
+    order = [j for j in np.lexsort((np.arange(256), -htr)) if lo <= H[j] <= hi]
+    rows = [plan.pivot_row[i] for i in range(4)]
+    gaps = np.abs(np.diff(np.sort(htr)))
+    if gaps.min() > 1e-6:
+        assert rows == order[:4]
+    for b in range(16):
+        j = plan.br_row[b]
+        assert plan.br_token[b] == b0["topk_id"][j, b % 4]
+    bt = stp.branch_tokens.cpu().numpy()
+    for b in range(16):
+        e = t0.copy()
+        e[plan.br_pos[b]] = plan.br_token[b]
+        assert np.array_equal(bt[b], e)
+    # the decision is the largest margin; commit iff positive
+    dec = P.read_decision(stp.dec)
+    deltas = stp.deltas.cpu().numpy()
+    assert dec.branch == int(np.argmax(deltas))
+    assert bool(dec.commit) == bool(deltas.max() > 0)
+    # every branch statistic is finite and the entropies are below log(V - 1)
+    bs = stp.branch_stats.numpy()
+    assert np.all(np.isfinite(bs["H"])) and np.all(bs["H"] <= np.log(B8.vocab - 1) + 1e-3)
+    # commit / carry-over
+    t1 = stp.tokens.cpu().numpy()
+    if dec.commit:
+        assert t1[dec.pivot_pos] == dec.token and stp.n_m == 255
+        keep = [j for j in range(256) if j != dec.pivot_row]
+        assert np.array_equal(stp.base.H.cpu().numpy()[:255], bs["H"][dec.branch * 256:(dec.branch + 1) * 256][keep])
+    else:
+        assert np.array_equal(t1, t0) and stp.n_m == 256

@@ -1,0 +1,361 @@
+"""GPU parity at small sizes that span several tiles and ragged tails: every
+C-ABI call against the CPU oracle on the same seeded inputs."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from synth import ModelShape
+from oracle import model as om
+from oracle import rps as orps
+from oracle.stats import softmax_stats
+from tests.parity import compare_stats, MARGIN
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+# 2-layer bf16 model with head_dim 128, a 512 residual and a vocabulary that is
+# not a multiple of the 256-token LM-head tile
+SMALL_BF16 = ModelShape(n_layers=2, d_model=512, n_heads=4, head_dim=128, d_ffn=1536, vocab=3000)
+
+
+@pytest.fixture(scope="module")
+def P():
+    import paper_2608_11742_amd as P
+    return P
+
+
+def _upload(w_np, dtype):
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    return {k: torch.from_numpy(v).to(DEV).to(td).contiguous() for k, v in w_np.items()}
+
+
+@pytest.fixture(scope="module")
+def tiny(P):
+    shape = synth.TINY
+    w_np = synth.model_weights_np(shape, seed=0, dtype="f32")
+    m = P.Model(shape, _upload(w_np, "f32"), dtype="f32", max_pos=256)
+    yield shape, w_np, m
+    m.close()
+
+
+@pytest.fixture(scope="module")
+def small_bf16(P):
+    shape = SMALL_BF16
+    w_np = synth.model_weights_np(shape, seed=0, dtype="bf16")
+    m = P.Model(shape, _upload(w_np, "bf16"), dtype="bf16", max_pos=512)
+    yield shape, w_np, m
+    m.close()
+
+
+# ------------------------------------------------------------ vocab_entropy_topk
+
+@pytest.mark.parametrize("dtype,R,d,V,tol", [("f32", 300, 256, 1000, 1e-4), ("bf16", 200, 512, 3000, 1e-3),
+                                             ("bf16", 1, 64, 300, 1e-3)])
+def test_vocab_entropy_topk(P, dtype, R, d, V, tol):
+    h = synth.hidden_np(11, "h", (R, d), dtype=dtype)
+    w = synth.weight_np(12, "w", (V, d), std=0.1, dtype=dtype)
+    rs = (0.5 + 4.0 * synth.uniform01_np(13, "rs", R)).astype(np.float32)
+    mask = V - 7
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    out = P.Stats(R, 16, device=DEV).fill_(float("nan"))
+    ws = torch.full((P.vocab_entropy_topk_workspace_bytes(R, V),), 255, dtype=torch.uint8, device=DEV)
+    P.vocab_entropy_topk(torch.from_numpy(h).to(DEV).to(td), torch.from_numpy(w).to(DEV).to(td), out, ws,
+                         row_scale=torch.from_numpy(rs).to(DEV), scale=1.5, mask_id=mask)
+    torch.cuda.synchronize()
+    logits = 1.5 * rs.astype(np.float64)[:, None] * (h.astype(np.float64) @ w.astype(np.float64).T)
+    logits[:, mask] = -np.inf
+    ref = softmax_stats(logits, 16)
+    rep = compare_stats(out.numpy(), ref, tol, label=f"vocab_entropy_topk {dtype}")
+    assert not np.any(out.numpy()["topk_id"] == mask)
+    print(rep)
+
+
+def test_vocab_entropy_topk_is_deterministic_and_ignores_workspace_contents(P):
+    R, d, V = 130, 256, 777
+    h = torch.from_numpy(synth.hidden_np(1, "h", (R, d), dtype="f32")).to(DEV)
+    w = torch.from_numpy(synth.weight_np(2, "w", (V, d), std=0.1, dtype="f32")).to(DEV)
+    n = P.vocab_entropy_topk_workspace_bytes(R, V)
+    outs = []
+    for fill in (0, 255):
+        out = P.Stats(R, 16, device=DEV)
+        ws = torch.full((n,), fill, dtype=torch.uint8, device=DEV)
+        P.vocab_entropy_topk(h, w, out, ws, mask_id=-1)
+        outs.append(out.numpy())
+    for key in outs[0]:
+        assert np.array_equal(outs[0][key], outs[1][key]), key
+
+
+# ------------------------------------------------------------ dllm_forward
+
+def test_forward_tiny_f32_ragged_batch(P, tiny):
+    shape, w_np, model = tiny
+    B_, S = 3, 50
+    toks = synth.tokens_np(3, "toks", B_ * S, shape.vocab).reshape(B_, S)
+    toks[:, 30:] = shape.mask_id
+    lm_pos = np.array([0, 7, 29, 30, 31, 40, 45, 49], dtype=np.int32)
+    scales = (1.0 + 6.0 * synth.uniform01_np(4, "s", S)).astype(np.float32)
+    out = model.forward(torch.from_numpy(toks).to(DEV), torch.from_numpy(lm_pos).to(DEV),
+                        row_scale=torch.from_numpy(scales).to(DEV), scale=2.0)
+    torch.cuda.synchronize()
+    logits = om.forward_logits(toks, w_np, shape, lm_pos, row_scale=scales[lm_pos], scale=2.0)
+    ref = softmax_stats(logits.reshape(-1, shape.vocab), 16)
+    print(compare_stats(out.numpy(), ref, 1e-4, label="forward tiny f32"))
+
+
+def test_forward_small_bf16_against_mirror(P, small_bf16):
+    shape, w_np, model = small_bf16
+    B_, S = 2, 136
+    toks = synth.tokens_np(5, "toks", B_ * S, shape.vocab - 1).reshape(B_, S)
+    toks[:, 70:] = shape.mask_id
+    lm_pos = np.arange(64, 136, dtype=np.int32)
+    out = model.forward(torch.from_numpy(toks).to(DEV), torch.from_numpy(lm_pos).to(DEV), scale=3.0)
+    torch.cuda.synchronize()
+    logits = om.forward_logits(toks, w_np, shape, lm_pos, scale=3.0, mirror=True)
+    ref = softmax_stats(logits.reshape(-1, shape.vocab), 16)
+    print(compare_stats(out.numpy(), ref, 2e-2, label="forward small bf16"))
+
+
+def test_cached_prefix_forward_tiny(P, tiny):
+    shape, w_np, model = tiny
+    Pn, Bk, nb = 40, 24, 3
+    prefix = synth.tokens_np(6, "prefix", Pn, shape.vocab - 1)
+    k, vt, cap = model.new_kv_cache(Pn)
+    from paper_2608_11742_amd._abi import KvCache
+    kvc = KvCache(k.data_ptr(), vt.data_ptr(), 0, cap)
+    model.forward(torch.from_numpy(prefix).to(DEV)[None], torch.arange(1, dtype=torch.int32, device=DEV),
+                  kv_out=kvc)
+    blocks = synth.tokens_np(7, "blocks", nb * Bk, shape.vocab).reshape(nb, Bk)
+    blocks[:, 5:] = shape.mask_id
+    lm = np.arange(Bk, dtype=np.int32)
+    kvc.len = Pn
+    out = model.forward(torch.from_numpy(blocks).to(DEV), torch.from_numpy(lm).to(DEV), pos_offset=Pn,
+                        kv_prefix=kvc, scale=4.0)
+    torch.cuda.synchronize()
+    kv = om.prefix_cache(prefix, w_np, shape)
+    for l in range(shape.n_layers):
+        assert np.max(np.abs(k[l, :, :Pn].cpu().numpy() - kv[l][0])) < 1e-4
+        assert np.max(np.abs(vt[l, :, :, :Pn].cpu().numpy().transpose(0, 2, 1) - kv[l][1])) < 1e-4
+    refs = []
+    for b in range(nb):
+        h = om.hidden(blocks[b], w_np, shape, pos_offset=Pn, prefix_kv=kv)
+        refs.append(om.lm_logits(h, w_np, shape, scale=4.0))
+    ref = softmax_stats(np.concatenate(refs), 16)
+    print(compare_stats(out.numpy(), ref, 1e-4, label="cached forward"))
+
+
+def test_probe_logits(P, tiny):
+    shape, w_np, model = tiny
+    S = 64
+    toks = synth.tokens_np(8, "t", S, shape.vocab - 1)
+    lm_pos = np.arange(32, 64, dtype=np.int32)
+    rows = np.array([0, 5, 31], dtype=np.int32)
+    tk = np.array([3, 1000, 17], dtype=np.int32)
+    pl = torch.zeros(3, dtype=torch.float32, device=DEV)
+    from paper_2608_11742_amd._abi import Probe
+    rows_d, tk_d = torch.from_numpy(rows).to(DEV), torch.from_numpy(tk).to(DEV)
+    scales = np.linspace(1, 3, S).astype(np.float32)
+    model.forward(torch.from_numpy(toks).to(DEV)[None], torch.from_numpy(lm_pos).to(DEV),
+                  row_scale=torch.from_numpy(scales).to(DEV), scale=2.0,
+                  probe=Probe(rows_d.data_ptr(), tk_d.data_ptr(), pl.data_ptr(), 3))
+    torch.cuda.synchronize()
+    logits = om.forward_logits(toks[None], w_np, shape, lm_pos, row_scale=scales[lm_pos], scale=2.0)[0]
+    assert np.allclose(pl.cpu().numpy(), logits[rows, tk], atol=1e-4)
+
+
+# ------------------------------------------------------------ scheduler kernels on planted statistics
+
+def _planted(n, V, seed, scale_lo=0.3, scale_hi=6.0):
+    rng = np.random.default_rng(seed)
+    sc = np.exp(rng.uniform(np.log(scale_lo), np.log(scale_hi), n))
+    logits = (rng.normal(0, 1, (n, V)) * sc[:, None]).astype(np.float32).astype(np.float64)
+    logits[:, V - 1] = -np.inf
+    ref = softmax_stats(logits, 16)
+    return ref
+
+
+def _to_dev_stats(P, ref):
+    st = P.Stats(len(ref), 16, device=DEV)
+    st.H.copy_(torch.from_numpy(ref.H.astype(np.float32)))
+    st.lse.copy_(torch.from_numpy(ref.lse.astype(np.float32)))
+    st.lmax.copy_(torch.from_numpy(ref.lmax.astype(np.float32)))
+    st.argmax.copy_(torch.from_numpy(ref.argmax.astype(np.int32)))
+    st.topk_id.copy_(torch.from_numpy(ref.topk_id.astype(np.int32)))
+    st.topk_logit.copy_(torch.from_numpy(ref.topk_logit.astype(np.float32)))
+    return st
+
+
+def _as_f32(ref):
+    """The oracle's view of statistics that were stored as float32."""
+    f = lambda a: a.astype(np.float32).astype(np.float64)
+    return orps.Stats(f(ref.H), f(ref.lse), f(ref.lmax), ref.argmax, ref.topk_id, f(ref.topk_logit))
+
+
+@pytest.mark.parametrize("mode,n,seed", [("band", 256, 0), ("band", 37, 1), ("paper", 200, 2), ("paper", 2, 3),
+                                         ("band", 1000, 4)])
+def test_select_pivots_matches_oracle(P, mode, n, seed):
+    ref = _planted(n, 400, seed, scale_hi=12.0)
+    st = _to_dev_stats(P, ref)
+    m_pos = np.sort(np.random.default_rng(seed).choice(5000, n, replace=False)).astype(np.int32)
+    prm_o = orps.Params(mode=mode, k_max=10, tau_pivot=0.9, n_pivots=4 if mode == "band" else 1,
+                        r=0.0 if mode == "band" else 0.1, n_cand=4 if mode == "band" else 10, max_branch=15)
+    prm = P.params(mode=mode, k_max=prm_o.k_max, tau_pivot=prm_o.tau_pivot, n_pivots=prm_o.n_pivots, r=prm_o.r,
+                   n_cand=prm_o.n_cand, max_branch=prm_o.max_branch)
+    plan = P.new_plan(DEV)
+    P.rps_select_pivots(st, torch.from_numpy(m_pos).to(DEV), n, prm, plan)
+    got = P.read_plan(plan)
+    exp = orps.select_pivots(_as_f32(ref), m_pos, prm_o)
+    margins_ok = all(min(p.feas_margin, p.rank_margin, p.cand_margin) > MARGIN for p in exp.pivots)
+    if not margins_ok:
+        pytest.skip("a pivot decision of this seed sits within the margin")
+    assert got.n_pivots == len(exp.pivots)
+    assert [got.pivot_pos[i] for i in range(got.n_pivots)] == [p.pos for p in exp.pivots]
+    brs = exp.branches()
+    assert got.n_branch == len(brs)
+    for b, (pi, row, pos, tok, lp) in enumerate(brs):
+        assert (got.br_pivot[b], got.br_row[b], got.br_pos[b], got.br_token[b]) == (pi, row, pos, tok)
+        assert abs(got.br_logp[b] - lp) < 1e-5
+
+
+def test_build_branches(P):
+    ref = _planted(64, 300, 5)
+    st = _to_dev_stats(P, ref)
+    S = 100
+    toks = synth.tokens_np(9, "t", S, 299)
+    m_pos = np.arange(36, 100, dtype=np.int32)
+    toks[m_pos] = 299
+    plan = P.new_plan(DEV)
+    P.rps_select_pivots(st, torch.from_numpy(m_pos).to(DEV), 64, P.params(mode="band", n_pivots=3, r=0.0, n_cand=4),
+                        plan)
+    got_plan = P.read_plan(plan)
+    out = torch.full((14, S), -7, dtype=torch.int32, device=DEV)
+    P.rps_build_branches(torch.from_numpy(toks).to(DEV), plan, True, 14, out)
+    o = out.cpu().numpy()
+    assert np.array_equal(o[0], toks)
+    for b in range(got_plan.n_branch):
+        e = toks.copy()
+        e[got_plan.br_pos[b]] = got_plan.br_token[b]
+        assert np.array_equal(o[1 + b], e)
+    for s in range(1 + got_plan.n_branch, 14):
+        assert np.array_equal(o[s], toks)
+
+
+@pytest.mark.parametrize("lam,offset,seed", [(0.0, 0, 0), (0.3, 1, 1), (0.1, 0, 2)])
+def test_lookahead_score_matches_oracle(P, lam, offset, seed):
+    n, V = 120, 300
+    anchor = _planted(n, V, 100 + seed)
+    rng = np.random.default_rng(seed)
+    plan_o = orps.select_pivots(_as_f32(anchor), np.arange(n), orps.Params(mode="band", n_pivots=4, r=0.0,
+                                                                            n_cand=4))
+    nb = len(plan_o.branches())
+    bstats = [_planted(n, V, 200 + 17 * seed + b) for b in range(nb)]
+    allst = ([anchor] if offset else []) + bstats
+    cat = orps.Stats.concat(allst)
+    dev_anchor = _to_dev_stats(P, anchor)
+    dev_br = _to_dev_stats(P, cat)
+    plan = P.new_plan(DEV)
+    P.rps_select_pivots(dev_anchor, torch.arange(n, dtype=torch.int32, device=DEV), n,
+                        P.params(mode="band", n_pivots=4, r=0.0, n_cand=4), plan)
+    dec = P.new_decision(DEV)
+    scores = torch.zeros(16, device=DEV)
+    deltas = torch.zeros(16, device=DEV)
+    P.rps_lookahead_score(dev_anchor, dev_br, offset, n, plan, lam, dec, scores=scores, deltas=deltas)
+    got = P.read_decision(dec)
+    exp = orps.score(_as_f32(anchor), [_as_f32(b) for b in bstats], plan_o, lam)
+    assert np.allclose(scores.cpu().numpy()[:nb], exp.scores, atol=2e-5)
+    assert np.allclose(deltas.cpu().numpy()[:nb], exp.deltas, atol=2e-5)
+    if exp.margin_sum > MARGIN:
+        assert bool(got.commit) == exp.commit and got.branch == exp.branch
+        assert got.pivot_pos == exp.pivot_pos and got.token == exp.token
+
+
+@pytest.mark.parametrize("tau,with_dec,seed", [(0.9, False, 0), (0.5, True, 1), (-1.0, True, 2), (0.999, False, 3)])
+def test_commit_matches_oracle(P, tau, with_dec, seed):
+    n, V, S = 50, 200, 90
+    base = _planted(n, V, 300 + seed, scale_hi=30.0)
+    m_pos = np.sort(np.random.default_rng(seed).choice(np.arange(40, 90), n, replace=False)).astype(np.int32)
+    toks = synth.tokens_np(seed, "t", S, V - 1)
+    toks[m_pos] = V - 1
+    state = orps.State(toks.astype(np.int64), m_pos.astype(np.int64), _as_f32(base))
+    dev_base = _to_dev_stats(P, base)
+    dec = None
+    br_dev = None
+    committed_expect = []
+    if with_dec:
+        plan_o = orps.select_pivots(_as_f32(base), m_pos, orps.Params(mode="band", n_pivots=2, r=0.0, n_cand=3))
+        nb = len(plan_o.branches())
+        bst = [_planted(n, V, 400 + b, scale_hi=30.0) for b in range(nb)]
+        d = orps.score(_as_f32(base), [_as_f32(b) for b in bst], plan_o, 0.0)
+        committed_expect += orps.apply_decision(state, d, [_as_f32(b) for b in bst], _as_f32(base))
+        plan = P.new_plan(DEV)
+        P.rps_select_pivots(dev_base, torch.from_numpy(m_pos).to(DEV), n,
+                            P.params(mode="band", n_pivots=2, r=0.0, n_cand=3), plan)
+        br_dev = _to_dev_stats(P, orps.Stats.concat(bst))
+        dec = P.new_decision(DEV)
+        P.rps_lookahead_score(dev_base, br_dev, 0, n, plan, 0.0, dec)
+        if d.margin_sum <= MARGIN:
+            pytest.skip("decision within the margin")
+    if tau >= 0:
+        rows, _, cmargin = orps.confidence_commit(state.stats, tau)
+        if cmargin <= MARGIN:
+            pytest.skip("confidence decision within the margin")
+        committed_expect += list(orps.apply_confidence_commit(state, tau, V - 1)[0])
+    t_dev = torch.from_numpy(toks).to(DEV)
+    m_dev = torch.from_numpy(m_pos).to(DEV)
+    n_out = torch.zeros(1, dtype=torch.int32, device=DEV)
+    comm = torch.full((n,), -1, dtype=torch.int32, device=DEV)
+    n_comm = torch.zeros(1, dtype=torch.int32, device=DEV)
+    P.rps_commit(t_dev, m_dev, n, dev_base, tau, n_out, comm, n_comm, dec=dec, branches=br_dev, branch_offset=0)
+    k = int(n_out.item())
+    assert k == len(state.m_pos)
+    assert np.array_equal(t_dev.cpu().numpy(), state.tokens)
+    assert np.array_equal(m_dev.cpu().numpy()[:k], state.m_pos)
+    nc = int(n_comm.item())
+    assert sorted(comm.cpu().numpy()[:nc].tolist()) == sorted(int(c) for c in committed_expect)
+    got = dev_base.numpy()
+    assert np.array_equal(got["H"][:k], state.stats.H.astype(np.float32))
+    assert np.array_equal(got["topk_id"][:k], state.stats.topk_id)
+
+
+# ------------------------------------------------------------ one RPS step end to end
+
+def test_tiny_rps_step_matches_oracle(P, tiny):
+    shape, w_np, model = tiny
+    wl = synth.WORKLOADS["tiny_rps_step_f32"]
+    prompt = synth.tokens_np(1, "prompt", wl.prompt_len, shape.vocab - 1)
+    toks = np.concatenate([prompt, np.full(wl.gen_len, shape.mask_id, np.int32)])
+    m_pos = np.arange(wl.prompt_len, wl.seq, dtype=np.int32)
+    t_dev, m_dev = torch.from_numpy(toks).to(DEV), torch.from_numpy(m_pos).to(DEV)
+    base = model.forward(t_dev[None], m_dev, scale=wl.logit_scale)
+    prm_o = orps.Params(mode="band", k_max=wl.k_max, n_pivots=wl.n_pivots, r=wl.r, n_cand=wl.n_cand,
+                        max_branch=wl.capacity)
+    prm = P.params(mode="band", k_max=wl.k_max, n_pivots=wl.n_pivots, r=wl.r, n_cand=wl.n_cand,
+                   max_branch=wl.capacity)
+    stp = P.RpsStep(model, t_dev, m_dev, base, prm, lam=wl.lam, capacity=wl.capacity, scale=wl.logit_scale)
+    stp.run()
+    torch.cuda.synchronize()
+
+    ref_base = softmax_stats(om.forward_logits(toks[None], w_np, shape, m_pos, scale=wl.logit_scale)[0], 16)
+    plan = orps.select_pivots(ref_base, m_pos, prm_o)
+    got_plan = P.read_plan(stp.plan)
+    assert [got_plan.pivot_pos[i] for i in range(got_plan.n_pivots)] == [p.pos for p in plan.pivots]
+    lg = om.forward_logits(orps.branch_tokens(toks, plan), w_np, shape, m_pos, scale=wl.logit_scale)
+    bst = [softmax_stats(l, 16) for l in lg]
+    got_br = stp.branch_stats.numpy()
+    ref_br = orps.Stats.concat(bst)
+    n_m = len(m_pos)
+    nb = len(bst)
+    compare_stats({k: v[:nb * n_m] for k, v in got_br.items()}, ref_br, 1e-4, label="branch stats")
+    dec = orps.score(ref_base, bst, plan, wl.lam)
+    gd = P.read_decision(stp.dec)
+    assert np.allclose(stp.deltas.cpu().numpy()[:nb], dec.deltas, atol=1e-5)
+    if dec.margin_sum > MARGIN:
+        assert bool(gd.commit) == dec.commit and gd.branch == dec.branch
+        state = orps.State(toks.astype(np.int64), m_pos.astype(np.int64), ref_base)
+        orps.apply_decision(state, dec, bst, ref_base)
+        assert np.array_equal(stp.tokens.cpu().numpy(), state.tokens)
+        assert stp.n_m == len(state.m_pos)
+        assert np.array_equal(stp.m_pos.cpu().numpy()[:stp.n_m], state.m_pos)
+        assert np.max(np.abs(stp.base.H.cpu().numpy()[:stp.n_m] - state.stats.H)) < 1e-4

@@ -293,3 +293,15 @@ def test_commit_and_carry_over():
         assert np.array_equal(st.stats.H, bst[dec.branch].H[keep])
     else:
         assert committed == [] and np.array_equal(st.m_pos, m_pos)
+
+
+def test_branch_capacity_truncates_then_drops():
+    rng = np.random.default_rng(9)
+    logits = rng.normal(0, 1, (12, V))
+    logits[:, MASK] = -np.inf
+    st = softmax_stats(logits, 16)
+    prm = rps.Params(mode="band", pct_lo=0, pct_hi=100, n_pivots=4, r=0.0, n_cand=4, max_branch=9)
+    plan = rps.select_pivots(st, np.arange(12), prm)
+    # 4 + 4 fit, the third pivot keeps 1 candidate and is dropped, the fourth has none
+    assert [len(p.tokens) for p in plan.pivots] == [4, 4]
+    assert len(plan.branches()) == 8
