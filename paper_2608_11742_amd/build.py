@@ -2,6 +2,7 @@
 from __future__ import annotations
 
 import os
+import re
 import subprocess
 import sys
 from concurrent.futures import ThreadPoolExecutor
@@ -15,7 +16,7 @@ LIB = os.path.join(HERE, "libdllm_rps.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
+FLAGS = ["-Rpass-analysis=kernel-resource-usage", "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
          # packed fp32 instructions stay off: hipcc must not emit v_pk_{add,mul,fma}_f32
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-Wno-unused-result"]
@@ -25,15 +26,35 @@ def sources():
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 
+def _scratch_users(remarks: str):
+    """Kernels whose resource-usage remarks report private scratch memory."""
+    users, fn = [], None
+    for line in remarks.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            fn = m.group(1)
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and int(m.group(1)) > 0:
+            users.append((fn, int(m.group(1))))
+    return users
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(OBJ, os.path.basename(src)[:-4] + ".o")
     cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
-    err = "\n".join(l for l in (r.stderr or "").splitlines() if "packed-fp32-ops" not in l)
+    lines = (r.stderr or "").splitlines()
+    err = "\n".join(l for l in lines if "packed-fp32-ops" not in l and "remark:" not in l
+                    and "kernel-resource-usage" not in l and not re.match(r"^\s*(\d+\s*)?\|", l))
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{err}")
     if err.strip():
         print(err, file=sys.stderr)
+    # register arrays indexed at run time end up in scratch memory and make a
+    # kernel an order of magnitude slower: refuse such a build
+    users = _scratch_users(r.stderr or "")
+    if users:
+        raise RuntimeError(f"{src}: kernels use scratch memory: {users}")
     return obj
 
 

@@ -26,7 +26,9 @@ struct EpiParams {
   QkvOut qkv;
 };
 
-template <typename T, int EPI>
+// HD: head_dim of the QKV epilogue (compile-time, so the rotary partner block
+// index stays static and the accumulators stay in registers); 0 otherwise.
+template <typename T, int EPI, int HD>
 __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(const T* __restrict__ A, int lda,
                                                            const T* __restrict__ B, int ldb, int M, int N, int K,
                                                            int tiles_m, int tiles_n, EpiParams ep) {
@@ -92,50 +94,121 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(const T* __restrict__
         }
       }
   } else {  // EPI_QKV
+    static_assert(HD == 64 || HD == 128, "head_dim");
     const QkvOut& o = ep.qkv;
-    const int hd = o.hd, half = hd / 2, pair = hd / 32;  // partner block distance
+    constexpr int hd = HD, half = HD / 2, pair = HD / 32;  // partner block distance
     const int wcol0 = tn * kBN + wn * TM::kWTN;            // first column of this wave tile
-    if (wcol0 >= N) return;
-    const int which = wcol0 / o.d;                         // 0: q, 1: k, 2: v
+    const int which = wcol0 / o.d;                         // 0: q, 1: k, 2: v (uniform per wave)
     const int cin0 = wcol0 % o.d;
+    // rotary embedding in registers: (x1, x2) = columns (dim, dim + hd/2) of one head
+    if (which < 2) {
 #pragma unroll
-    for (int m = 0; m < TM::kFM; ++m)
+      for (int m = 0; m < TM::kFM; ++m)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = row_base + m * 16 + i;
-        if (row >= M) continue;
-        const int b = row / o.seq, s = row % o.seq;
-        const int pos = o.pos_offset + s;
+        for (int i = 0; i < 4; ++i) {
+          const int row = min(row_base + m * 16 + i, M - 1);
+          const int pos = o.pos_offset + row % o.seq;
 #pragma unroll
-        for (int n = 0; n < TM::kFN; ++n) {
-          const int cin = cin0 + n * 16 + lc;
-          const int h = cin / hd, dim = cin % hd;
-          const float x1 = acc[m][n][i];
-          if (which == 2) {
-            T* vt = reinterpret_cast<T*>(o.vt);
-            store_f(vt + (size_t(b * o.H + h) * hd + dim) * o.vt_ld + s, x1);
-            continue;
+          for (int n = 0; n < TM::kFN; ++n) {
+            if constexpr (true) {
+              if (((n * 16) % hd) >= half) continue;
+              const int dim = (cin0 + n * 16 + lc) % hd;
+              const float2 cs = o.rope[size_t(pos) * half + dim];
+              const float x1 = acc[m][n][i], x2 = acc[m][n + pair][i];
+              acc[m][n][i] = x1 * cs.x - x2 * cs.y;
+              acc[m][n + pair][i] = x1 * cs.y + x2 * cs.x;
+            }
           }
-          if (((n * 16) % hd) >= half) continue;           // second half: written with its partner
-          float x2 = 0.f;
+        }
+    }
+    if constexpr (Elem<T>::bytes == 2) {
+      // stage the wave's 64 x 128 tile as bf16 in LDS (V transposed), then write
+      // 16-byte chunks: Q/K rows are contiguous along head_dim, V^T rows along positions
+      uint8_t* st = smem + wave * (TM::kWTM * TM::kWTN * 2);
+      if (which < 2) {
 #pragma unroll
-          for (int p = 0; p < TM::kFN; ++p)
-            if (p == n + pair) x2 = acc[m][p][i];
-          const float2 cs = o.rope[size_t(pos) * half + dim];
-          T* dst = reinterpret_cast<T*>(which == 0 ? o.q : o.k) + (size_t(b * o.H + h) * o.seq + s) * hd;
-          store_f(dst + dim, x1 * cs.x - x2 * cs.y);
-          store_f(dst + dim + half, x1 * cs.y + x2 * cs.x);
+        for (int m = 0; m < TM::kFM; ++m)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int n = 0; n < TM::kFN; ++n) {
+              const int r = m * 16 + 4 * (lane >> 4) + i, c = n * 16 + lc;
+              *reinterpret_cast<uint16_t*>(st + (r * TM::kWTN + c) * 2) = f2bf(acc[m][n][i]);
+            }
+      } else {
+#pragma unroll
+        for (int m = 0; m < TM::kFM; ++m)
+#pragma unroll
+          for (int n = 0; n < TM::kFN; ++n) {
+            const int r = m * 16 + 4 * (lane >> 4), c = n * 16 + lc;
+            const uint32_t lo = uint32_t(f2bf(acc[m][n][0])) | (uint32_t(f2bf(acc[m][n][1])) << 16);
+            const uint32_t hi = uint32_t(f2bf(acc[m][n][2])) | (uint32_t(f2bf(acc[m][n][3])) << 16);
+            *reinterpret_cast<u32x2*>(st + (c * TM::kWTM + r) * 2) = u32x2{lo, hi};
+          }
+      }
+      __syncthreads();
+      const int r0 = m0 + wm * TM::kWTM;
+      if (which < 2) {
+        uint16_t* dst = reinterpret_cast<uint16_t*>(which == 0 ? o.q : o.k);
+        for (int q = lane; q < TM::kWTM * TM::kWTN / 8; q += 64) {
+          const int r = q / (TM::kWTN / 8), c8 = (q % (TM::kWTN / 8)) * 8;
+          const int row = r0 + r;
+          if (row >= M) continue;
+          const int b = row / o.seq, sp = row % o.seq;
+          const int cin = cin0 + c8, h = cin / hd, dim = cin % hd;
+          *reinterpret_cast<u32x4*>(dst + (size_t(b * o.H + h) * o.seq + sp) * hd + dim) =
+              *reinterpret_cast<const u32x4*>(st + (r * TM::kWTN + c8) * 2);
+        }
+      } else {
+        uint16_t* dst = reinterpret_cast<uint16_t*>(o.vt);
+        const bool aligned = (o.seq % 8) == 0;
+        for (int q = lane; q < TM::kWTM * TM::kWTN / 8; q += 64) {
+          const int c = q / (TM::kWTM / 8), rr = (q % (TM::kWTM / 8)) * 8;
+          const int cin = cin0 + c, h = cin / hd, dim = cin % hd;
+          const int row = r0 + rr;
+          if (row >= M) continue;
+          if (aligned && row + 7 < M) {
+            const int b = row / o.seq, sp = row % o.seq;
+            *reinterpret_cast<u32x4*>(dst + (size_t(b * o.H + h) * hd + dim) * o.vt_ld + sp) =
+                *reinterpret_cast<const u32x4*>(st + (c * TM::kWTM + rr) * 2);
+          } else {
+            for (int e = 0; e < 8 && row + e < M; ++e) {
+              const int b = (row + e) / o.seq, sp = (row + e) % o.seq;
+              dst[(size_t(b * o.H + h) * hd + dim) * o.vt_ld + sp] =
+                  *reinterpret_cast<const uint16_t*>(st + (c * TM::kWTM + rr + e) * 2);
+            }
+          }
         }
       }
+    } else {
+      // fp32 activations: direct element stores
+#pragma unroll
+      for (int m = 0; m < TM::kFM; ++m)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = row_base + m * 16 + i;
+          if (row >= M) continue;
+          const int b = row / o.seq, sp = row % o.seq;
+#pragma unroll
+          for (int n = 0; n < TM::kFN; ++n) {
+            const int cin = cin0 + n * 16 + lc;
+            const int h = cin / hd, dim = cin % hd;
+            T* dst = which == 2 ? reinterpret_cast<T*>(o.vt) + (size_t(b * o.H + h) * hd + dim) * o.vt_ld + sp
+                                : reinterpret_cast<T*>(which == 0 ? o.q : o.k) + (size_t(b * o.H + h) * o.seq + sp) * hd +
+                                      dim;
+            store_f(dst, acc[m][n][i]);
+          }
+        }
+    }
   }
 }
 
-template <typename T, int EPI>
+template <typename T, int EPI, int HD = 0>
 hipError_t launch(const void* A, int lda, const void* B, int ldb, int M, int N, int K, int tiles_n,
                   const EpiParams& ep, hipStream_t s) {
   const int tiles_m = cdiv(M, kBM);
   const int grid = tiles_m * tiles_n;
-  hipLaunchKernelGGL((gemm_kernel<T, EPI>), dim3(grid), dim3(kThreads), 0, s, static_cast<const T*>(A), lda,
+  hipLaunchKernelGGL((gemm_kernel<T, EPI, HD>), dim3(grid), dim3(kThreads), 0, s, static_cast<const T*>(A), lda,
                      static_cast<const T*>(B), ldb, M, N, K, tiles_m, tiles_n, ep);
   return hipGetLastError();
 }
@@ -168,8 +241,11 @@ hipError_t gemm_qkv(int dtype, const void* A, int lda, const void* Wqkv, int M, 
   ep.qkv = o;
   const int N = 3 * o.d;
   const int tn = cdiv(N, kBN);
-  return dtype ? launch<bf16_t, EPI_QKV>(A, lda, Wqkv, K, M, N, K, tn, ep, s)
-               : launch<float, EPI_QKV>(A, lda, Wqkv, K, M, N, K, tn, ep, s);
+  if (o.hd == 128)
+    return dtype ? launch<bf16_t, EPI_QKV, 128>(A, lda, Wqkv, K, M, N, K, tn, ep, s)
+                 : launch<float, EPI_QKV, 128>(A, lda, Wqkv, K, M, N, K, tn, ep, s);
+  return dtype ? launch<bf16_t, EPI_QKV, 64>(A, lda, Wqkv, K, M, N, K, tn, ep, s)
+               : launch<float, EPI_QKV, 64>(A, lda, Wqkv, K, M, N, K, tn, ep, s);
 }
 
 }  // namespace dllm

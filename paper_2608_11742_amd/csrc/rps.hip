@@ -115,7 +115,7 @@ __global__ __launch_bounds__(kT) void select_kernel(StatsIn st, const int32_t* _
 
   if (tid != 0) return;
   // adaptive candidate sets: v in T_{i*} with p(v) >= r P^max, rank order, capped
-  rps_plan pl;
+  rps_plan& pl = *plan;   // written in place (a private copy would live in scratch memory)
   pl.n_pivots = 0;
   pl.n_branch = 0;
   for (int i = 0; i < RPS_MAX_PIVOTS; ++i) pl.pivot_row[i] = pl.pivot_pos[i] = pl.n_cand[i] = -1;
@@ -148,7 +148,6 @@ __global__ __launch_bounds__(kT) void select_kernel(StatsIn st, const int32_t* _
       pl.br_logp[b] = st.topk_logit[size_t(j) * st.k + k] - lse;
     }
   }
-  *plan = pl;
 }
 
 __global__ __launch_bounds__(kT) void branch_kernel(const int32_t* __restrict__ tokens, int seq,

@@ -21,8 +21,15 @@ def determined_ranks(ref_logits: np.ndarray, kth_margin: np.ndarray, margin: flo
     return (gaps > margin) & (left > margin)
 
 
-def compare_stats(got: dict, ref, tol: float, k: int | None = None, margin: float = MARGIN, label: str = ""):
-    """Float fields within tol (max-abs); argmax and top-k ids equal where determined."""
+def compare_stats(got: dict, ref, tol: float, k: int | None = None, margin=MARGIN, label: str = ""):
+    """Float fields within tol (max-abs); argmax and top-k ids equal where determined.
+
+    margin="auto" (end-to-end bf16 comparisons, where the inputs of the LM head
+    already differ by rounding-order effects amplified through the layers):
+    decisions are compared where the oracle's margin exceeds
+    max(1e-3, 2 x the observed max-abs logit error); kernel-level comparisons
+    on identical inputs use the fixed 1e-3.
+    """
     k = k or ref.topk_id.shape[1]
     report = {}
     for name in ("H", "lse", "lmax"):
@@ -33,6 +40,9 @@ def compare_stats(got: dict, ref, tol: float, k: int | None = None, margin: floa
     tl_err = float(np.max(np.abs(got["topk_logit"][:, :k] - ref.topk_logit[:, :k])))
     report["topk_logit"] = tl_err
     assert tl_err <= tol, f"{label} topk_logit: max-abs error {tl_err:.3e} > {tol:.1e}"
+    if margin == "auto":
+        margin = max(MARGIN, 2.0 * max(tl_err, report["lmax"]))
+    report["margin"] = margin
     am = ref.argmax_margin > margin
     bad = np.nonzero(am & (got["argmax"] != ref.argmax))[0]
     assert bad.size == 0, f"{label} argmax mismatch at rows {bad[:8]}"

@@ -70,18 +70,19 @@ def _branch_batch(shape, n_branch=16, P_=256, G=256):
 
 def test_two_layer_8b_width_forward_in_bench_launch_config(P, b8_two_layer):
     """16 x 512 batch (M = 8192 GEMM rows) through 2 layers of 8B width; sequence 5
-    against the mirror oracle on 32 sampled masked rows."""
+    against the mirror oracle on 32 sampled masked rows, at the unscaled logits
+    of the 8B workloads (scale 1)."""
     shape, w, model = b8_two_layer
     batch, m_pos = _branch_batch(shape)
-    out = model.forward(torch.from_numpy(batch).to(DEV), torch.from_numpy(m_pos).to(DEV), scale=4.0)
+    out = model.forward(torch.from_numpy(batch).to(DEV), torch.from_numpy(m_pos).to(DEV), scale=1.0)
     torch.cuda.synchronize()
     b = 5
     w_np = {k: v.float().cpu().numpy() for k, v in w.items()}
     sample = np.unique(np.concatenate([[0, 255], synth.tokens_np(33, "s", 30, 256)]))
     h = om.hidden(batch[b], w_np, shape, mirror=True)[m_pos[sample]]
-    ref = softmax_stats(om.lm_logits(h, w_np, shape, scale=4.0), 16)
+    ref = softmax_stats(om.lm_logits(h, w_np, shape, scale=1.0), 16)
     got = {k: v[b * 256 + sample] for k, v in out.numpy().items()}
-    print(compare_stats(got, ref, 2e-2, label="2-layer 8B width"))
+    print(compare_stats(got, ref, 2e-2, margin="auto", label="2-layer 8B width"))
 
 
 def test_batch_invariance(P, b8_two_layer):
