@@ -12,7 +12,8 @@ namespace dllm {
 namespace {
 
 constexpr int kBM = 256, kBN = 256;
-using Tile = TileMma<bf16_t, kBM, kBN, 4, 2>;  // geometry is the same for fp32
+constexpr int kWavesM = 4, kWavesN = 2;   // 8 waves of 64 x 128, two per SIMD
+using Tile = TileMma<bf16_t, kBM, kBN, kWavesM, kWavesN>;  // geometry is the same for fp32
 constexpr int kThreads = Tile::kThreads;
 constexpr int kGroupM = 8;
 
@@ -32,7 +33,7 @@ template <typename T, int EPI, int HD>
 __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(const T* __restrict__ A, int lda,
                                                            const T* __restrict__ B, int ldb, int M, int N, int K,
                                                            int tiles_m, int tiles_n, EpiParams ep) {
-  using TM = TileMma<T, kBM, kBN, 4, 2>;
+  using TM = TileMma<T, kBM, kBN, kWavesM, kWavesN>;
   __shared__ __attribute__((aligned(16))) uint8_t smem[TM::kSmem];
   int tm, tn;
   map_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, kGroupM, tm, tn);
@@ -57,7 +58,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(const T* __restrict__
           K / TM::kKPerStage, acc);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave / 2, wn = wave % 2;
+  const int wm = wave / kWavesN, wn = wave % kWavesN;
   const int row_base = m0 + wm * TM::kWTM + 4 * (lane >> 4);
   const int lc = lane & 15;
 
