@@ -96,6 +96,88 @@ def cpu_baseline(wl, w_dev, tokens_np, m_pos_np, n_layers_sample=2, lm_rows_samp
             "sample_seconds": round(t_layers + t_lm, 2), "host_cpus": os.cpu_count()}
 
 
+def timed(fn, n):
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(n):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / n
+
+
+def other_configs(P, model, shape, n):
+    """The other 8B-shape configurations, on the same weights."""
+    from paper_2608_11742_amd._abi import KvCache
+    dev = torch.device("cuda:0")
+    out = {}
+    weights_gb = 2.0 * shape.n_params() / 1e9
+
+    # single denoising forward, 1 x 512, statistics on the 256 masked rows
+    wl = W.WORKLOADS["b8_forward_bf16"]
+    tokens, m_pos, base = build_state(P, model, wl, dev)
+    t = timed(lambda: model.forward(tokens[None], m_pos, out=base), n)
+    fl = step_flops(shape, 1, wl.seq, wl.gen_len)
+    out[wl.name] = {"forwards_per_s": round(1.0 / t, 2), "ms": round(t * 1e3, 3),
+                    "tflops": round(fl / t / 1e12, 1), "tflop": round(fl / 1e12, 2)}
+    log(f"{wl.name}: {t * 1e3:.2f} ms")
+
+    # KV-cached RPS step: 1024 cached prefix positions, 16 branch blocks of 32
+    wl = W.WORKLOADS["b8_cached_step_bf16"]
+    prefix = synth.tokens_torch(W.SEED_PROMPT, "prefix", wl.prompt_len, shape.vocab - 1, device=dev)
+    k, vt, cap = model.new_kv_cache(wl.prompt_len)
+    kv = KvCache(k.data_ptr(), vt.data_ptr(), 0, cap)
+    model.forward(prefix[None], torch.zeros(1, dtype=torch.int32, device=dev), kv_out=kv)
+    kv.len = wl.prompt_len
+    block = torch.full((wl.block,), shape.mask_id, dtype=torch.int32, device=dev)
+    bpos = torch.arange(wl.block, dtype=torch.int32, device=dev)
+    bbase = model.forward(block[None], bpos, pos_offset=wl.prompt_len, kv_prefix=kv)
+    snap = (block.clone(), bpos.clone(), bbase.numpy())
+    prm = P.params(mode=wl.pivot_mode, k_max=wl.k_max, n_pivots=wl.n_pivots, r=wl.r, n_cand=wl.n_cand,
+                   max_branch=wl.capacity)
+
+    def fresh():
+        block.copy_(snap[0])
+        bpos.copy_(snap[1])
+        for kk, v in snap[2].items():
+            getattr(bbase, kk).copy_(torch.from_numpy(v))
+        return P.RpsStep(model, block, bpos, bbase, prm, lam=wl.lam, capacity=wl.capacity, kv_prefix=kv,
+                         pos_offset=wl.prompt_len)
+    stp = fresh()
+    stp.run()
+    stp = fresh()
+    t = timed(stp.run, n)
+    rows = wl.capacity * wl.block
+    fl = shape.n_layers * (sum(linear_flops(shape, rows).values())
+                           + 4.0 * rows * (wl.prompt_len + wl.block) * shape.d_model) \
+        + 2.0 * rows * shape.d_model * shape.vocab
+    kv_gb = 2.0 * 2 * shape.n_layers * shape.n_heads * wl.prompt_len * shape.head_dim / 1e9
+    out[wl.name] = {"steps_per_s": round(1.0 / t, 2), "ms": round(t * 1e3, 3), "tflops": round(fl / t / 1e12, 1),
+                    "gbs": round((weights_gb + kv_gb) / t, 1),
+                    "algorithmic_gb": round(weights_gb + kv_gb, 2), "tflop": round(fl / 1e12, 2)}
+    log(f"{wl.name}: {t * 1e3:.2f} ms")
+
+    # full blockwise decode of 256 tokens (Algorithm 1)
+    wl = W.WORKLOADS["b8_decode_bf16"]
+    prompt = synth.tokens_torch(W.SEED_PROMPT, "prompt", wl.prompt_len, shape.vocab - 1, device=dev)
+    scales = torch.from_numpy(synth.position_scales_np(W.SEED_SCALE, np.arange(wl.seq), *wl.scale_range)).to(dev)
+    prm = P.params(mode="paper", k_max=wl.k_max, tau_pivot=wl.tau_pivot, n_pivots=1, r=wl.r, n_cand=wl.n_cand,
+                   max_branch=wl.capacity - 1)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    toks, st = P.rps_decode(model, prompt, wl.gen_len, wl.block, prm, wl.lam, wl.tau_conf,
+                            capacity=wl.capacity, row_scale=scales, timing=True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    out[wl.name] = {"committed_tokens_per_s": round(wl.gen_len / wall, 2), "wall_s": round(wall, 3),
+                    "nfe": st.nfe, "normal_forwards": st.normal, "lookahead_forwards": st.lookahead,
+                    "normal_ms_avg": round(st.normal_ms / max(1, st.normal), 2),
+                    "lookahead_ms_avg": round(st.lookahead_ms / max(1, st.lookahead), 2),
+                    "commits_confidence": st.commits_conf, "commits_pivot": st.commits_pivot,
+                    "abstains": st.abstains}
+    log(f"{wl.name}: {wall:.2f} s, NFE {st.nfe}")
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -104,6 +186,8 @@ def main():
     ap.add_argument("--workload", default="b8_rps_step_bf16", choices=["b8_rps_step_bf16"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layers", type=int, default=0, help="override layer count (profiling runs only)")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the other 8B configurations (single forward, cached step, full decode)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the lookahead branches would shard "
@@ -125,7 +209,8 @@ def main():
     torch.cuda.synchronize()
     log(f"weights generated on device in {time.perf_counter() - t:.1f} s "
         f"({shape.n_params() / 1e9:.2f} B params)")
-    model = P.Model(shape, w, dtype="bf16", max_pos=wl.seq)
+    max_pos = max(x.seq for x in W.WORKLOADS.values() if x.model == W.WORKLOADS["b8_rps_step_bf16"].model)
+    model = P.Model(shape, w, dtype="bf16", max_pos=max_pos)
     tokens, m_pos, base = build_state(P, model, wl, dev)
     prm = P.params(mode=wl.pivot_mode, k_max=wl.k_max, tau_pivot=wl.tau_pivot, pct_lo=wl.pct_lo,
                    pct_hi=wl.pct_hi, n_pivots=wl.n_pivots, r=wl.r, n_cand=wl.n_cand, max_branch=wl.capacity)
@@ -202,6 +287,8 @@ def main():
         },
         "kernels": kern,
     }
+    if not args.no_extras:
+        res["other_configs"] = other_configs(P, model, shape, args.steps)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle sample")
         res["cpu_baseline"] = cpu_baseline(wl, w, snap[0].cpu().numpy(), snap[1].cpu().numpy())

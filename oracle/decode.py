@@ -16,7 +16,10 @@ The loop itself only follows Algorithm 1:
           distributions, or abstain and carry the anchor's
 
 Every forward is counted (NFE), split into normal and lookahead passes as in
-the paper's speedup decomposition (Table 4).
+the paper's speedup decomposition (Table 4).  The trace records every
+decision with its margin (distance of the deciding value from its boundary):
+("commit", positions, margin), ("skip", margin), ("lookahead", pivot, token
+or -1 for abstain, margin).
 """
 from __future__ import annotations
 
@@ -58,9 +61,9 @@ def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps
         while len(state.m_pos) > 0:
             iters += 1
             assert iters <= max_iters
-            committed, _ = rps.apply_confidence_commit(state, tau, mask_id)
+            committed, cmargin = rps.apply_confidence_commit(state, tau, mask_id)
             res.commits_conf += len(committed)
-            res.trace.append(("commit", [int(c) for c in committed]))
+            res.trace.append(("commit", sorted(int(c) for c in committed), cmargin))
             if len(state.m_pos) == 0:
                 break
             plan = rps.select_pivots(state.stats, state.m_pos, prm)
@@ -70,7 +73,7 @@ def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps
                 state.stats = forward(state.tokens[None, :], state.m_pos, None)[0][0]
                 res.nfe += 1
                 res.normal += 1
-                res.trace.append(("skip",))
+                res.trace.append(("skip", plan.empty_margin))
                 continue
             pv = plan.pivots[0]
             batch = rps.branch_tokens(state.tokens, plan, with_anchor=True)
@@ -81,7 +84,9 @@ def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps
             anchor, anchor_probe = outs[0]
             branch_stats = [o[0] for o in outs[1:]]
             dec = rps.score(anchor, branch_stats, plan, lam, anchor_logp=anchor_probe)
-            res.trace.append(("lookahead", pv.pos, dec.token if dec.commit else -1))
+            pmargin = min(pv.feas_margin, pv.rank_margin, pv.cand_margin, plan.empty_margin)
+            res.trace.append(("lookahead", pv.pos, dec.token if dec.commit else -1,
+                              min(dec.margin_sum, pmargin)))
             if dec.commit:
                 res.commits_pivot += 1
             else:

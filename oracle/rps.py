@@ -58,6 +58,8 @@ class Pivot:
 @dataclass
 class Plan:
     pivots: list = field(default_factory=list)
+    # decision margin of an empty plan (distance of the nearest row from feasibility)
+    empty_margin: float = math.inf
 
     def branches(self):
         """(pivot index, pivot row, pivot pos, token, anchor logp) in pivot-major, rank order."""
@@ -140,7 +142,7 @@ def select_pivots(st: Stats, m_pos, prm: Params) -> Plan:
         raise ValueError(prm.mode)
     cand_rows = np.nonzero(feas)[0]
     if cand_rows.size == 0:
-        return Plan()
+        return Plan(empty_margin=float(np.min(feas_margin)))
     # rank feasible rows by truncated entropy, larger first, then lower position
     order = cand_rows[np.lexsort((m_pos[cand_rows], -htr[cand_rows]))]
     chosen = order[:prm.n_pivots]

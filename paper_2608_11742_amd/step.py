@@ -77,10 +77,13 @@ class DecodeStats:
 
 
 def rps_decode(model, prompt, gen_len: int, block: int, prm, lam: float, tau: float, capacity: int = 16,
-               row_scale=None, scale: float = 1.0, k: int = 16, timing: bool = False):
+               row_scale=None, scale: float = 1.0, k: int = 16, timing: bool = False, record: bool = False):
     """Algorithm 1 on the GPU.  prompt: [P] int32 device.  Returns (tokens, DecodeStats).
 
     row_scale: optional [P + gen_len] per-position logit scales (device float32).
+    record: keep a trace of every decision, ("commit", positions),
+    ("skip",) and ("lookahead", pivot, token or -1), at the cost of one more
+    read-back per standard commit.
     """
     if prm.max_branch > capacity - 1:
         raise ValueError("prm.max_branch must leave slot 0 of the lookahead batch to the anchor")
@@ -128,6 +131,8 @@ def rps_decode(model, prompt, gen_len: int, block: int, prm, lam: float, tau: fl
             B.rps_commit(tokens, m_pos, n_m, base, tau, n_m_out, committed, n_committed)   # standard commit
             n_new = int(n_m_out.item())
             st.commits_conf += n_m - n_new
+            if record:
+                st.trace.append(("commit", sorted(committed[:n_m - n_new].tolist())))
             n_m = n_new
             if n_m == 0:
                 break
@@ -135,7 +140,7 @@ def rps_decode(model, prompt, gen_len: int, block: int, prm, lam: float, tau: fl
             nb = B.read_plan(plan).n_branch
             if nb == 0:                                                  # skip rules: normal forward
                 fwd(tokens[None], n_m, base)
-                st.trace.append("skip")
+                st.trace.append(("skip",))
                 continue
             B.rps_build_branches(tokens, plan, True, 1 + nb, bt)
             probe = Probe(B.plan_field_ptr(plan, "br_row"), B.plan_field_ptr(plan, "br_token"),
@@ -146,11 +151,12 @@ def rps_decode(model, prompt, gen_len: int, block: int, prm, lam: float, tau: fl
             B.rps_commit(tokens, m_pos, n_m, base, -1.0, n_m_out, committed, n_committed, dec=dec,
                          branches=branch, branch_offset=1, anchor=anchor)
             n_new = int(n_m_out.item())
+            if record:
+                d = B.read_decision(dec)
+                st.trace.append(("lookahead", d.pivot_pos, d.token if d.commit else -1))
             if n_new < n_m:
                 st.commits_pivot += 1
-                st.trace.append("commit")
             else:
                 st.abstains += 1
-                st.trace.append("abstain")
             n_m = n_new
     return tokens, st

@@ -158,3 +158,31 @@ def test_full_step_properties(P, b8_full):
         assert np.array_equal(stp.base.H.cpu().numpy()[:255], bs["H"][dec.branch * 256:(dec.branch + 1) * 256][keep])
     else:
         assert np.array_equal(t1, t0) and stp.n_m == 256
+
+
+def test_cached_step_two_layer_8b_width(P, b8_two_layer):
+    """KV-cached lookahead (1024 cached prefix positions, 16 branch blocks of 32):
+    branch 7 against the mirror oracle with the oracle's own prefix cache."""
+    from paper_2608_11742_amd._abi import KvCache
+    shape, w, model = b8_two_layer
+    Pn, Bk, nb = 1024, 32, 16
+    model_p = P.Model(shape, w, dtype="bf16", max_pos=Pn + Bk)
+    prefix = synth.tokens_np(41, "prefix", Pn, shape.vocab - 1)
+    k, vt, cap = model_p.new_kv_cache(Pn)
+    kv = KvCache(k.data_ptr(), vt.data_ptr(), 0, cap)
+    model_p.forward(torch.from_numpy(prefix).to(DEV)[None], torch.zeros(1, dtype=torch.int32, device=DEV), kv_out=kv)
+    kv.len = Pn
+    blocks = np.full((nb, Bk), shape.mask_id, dtype=np.int32)
+    blocks[np.arange(nb), synth.tokens_np(42, "piv", nb, Bk)] = synth.tokens_np(43, "tok", nb, shape.vocab - 1)
+    lm = np.arange(Bk, dtype=np.int32)
+    out = model_p.forward(torch.from_numpy(blocks).to(DEV), torch.from_numpy(lm).to(DEV), pos_offset=Pn,
+                          kv_prefix=kv, scale=1.0)
+    torch.cuda.synchronize()
+    w_np = {kk: v.float().cpu().numpy() for kk, v in w.items()}
+    ref_kv = om.prefix_cache(prefix, w_np, shape, mirror=True)
+    b = 7
+    h = om.hidden(blocks[b], w_np, shape, pos_offset=Pn, mirror=True, prefix_kv=ref_kv)
+    ref = softmax_stats(om.lm_logits(h, w_np, shape, scale=1.0), 16)
+    got = {kk: v[b * Bk:(b + 1) * Bk] for kk, v in out.numpy().items()}
+    print(compare_stats(got, ref, 2e-2, margin="auto", label="cached step 2-layer 8B width"))
+    model_p.close()
