@@ -36,9 +36,46 @@ PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 METRIC = "denoising steps/sec and committed tokens/sec, 8B-shape, lookahead batch 16"
 
+# HBM bytes per launch of the gate/up projection kernel at the 16 x 512-row
+# step, from rocprofv3 FETCH_SIZE and WRITE_SIZE passes, each scaled by what
+# the same counter reads for a plain device copy of known size (the
+# --copy-calibration mode).  Valid only for the kernel sources they were
+# measured on: bench.py reports null once those files change.
+TRAFFIC_GATEUP = {"fetch_bytes": None, "write_bytes": None, "sources_sha256": None}
+TRAFFIC_SOURCES = ("paper_2608_11742_amd/csrc/gemm.hip", "paper_2608_11742_amd/csrc/mainloop.h",
+                   "paper_2608_11742_amd/csrc/common.h")
+
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_sources_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic():
+    t = TRAFFIC_GATEUP
+    if t["sources_sha256"] is None or t["sources_sha256"] != kernel_sources_sha256():
+        return None
+    return t["fetch_bytes"] + t["write_bytes"]
+
+
+def copy_calibration(mib):
+    """A plain device-to-device copy of a known number of bytes (3 launches),
+    the reference point that scales the HBM byte counters."""
+    n = int(mib) << 20
+    src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(7)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_per_launch": n, "launches": 3}), flush=True)
 
 
 def build_state(P, model, wl, dev):
@@ -188,6 +225,8 @@ def main():
     ap.add_argument("--layers", type=int, default=0, help="override layer count (profiling runs only)")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the other 8B configurations (single forward, cached step, full decode)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain copy of MIB mebibytes (scale for rocprofv3 byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the lookahead branches would shard "
@@ -196,6 +235,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     import paper_2608_11742_amd as P
 
     wl = W.WORKLOADS[args.workload]
@@ -282,7 +324,7 @@ def main():
         "roofline": {
             "bound": "mfma", "kernel": "gemm_gateup (gate/up projection + SwiGLU epilogue)",
             "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": recorded_traffic(),
             "flop_per_launch": lf[dom],
         },
         "kernels": kern,

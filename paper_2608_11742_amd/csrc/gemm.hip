@@ -207,6 +207,8 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(const T* __restrict__
 template <typename T, int EPI, int HD = 0>
 hipError_t launch(const void* A, int lda, const void* B, int ldb, int M, int N, int K, int tiles_n,
                   const EpiParams& ep, hipStream_t s) {
+  // the mainloop runs stages in pairs
+  if (K <= 0 || K % (2 * TileMma<T, kBM, kBN, kWavesM, kWavesN>::kKPerStage)) return hipErrorInvalidValue;
   const int tiles_m = cdiv(M, kBM);
   const int grid = tiles_m * tiles_n;
   hipLaunchKernelGGL((gemm_kernel<T, EPI, HD>), dim3(grid), dim3(kThreads), 0, s, static_cast<const T*>(A), lda,

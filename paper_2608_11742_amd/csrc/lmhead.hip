@@ -269,6 +269,7 @@ size_t lmhead_workspace(int R, int V) {
 hipError_t lmhead_partials(int dtype, const void* h, const void* w, int R, int d, int V, const float* row_scale,
                            const int32_t* rs_idx, int rs_n, int rs_lim, float scale, int mask_id, void* ws,
                            hipStream_t s) {
+  if (d <= 0 || d % (dtype ? 64 : 32)) return hipErrorInvalidValue;   // the mainloop runs stages in pairs
   const int ns = slices_for(R, V);
   const int rt = cdiv(R, kRows), vt = cdiv(V, kCols);
   Partials part = carve(ws, R, ns * kSegs);

@@ -10,12 +10,14 @@
 // work to land; the MMA fragments of the next stage are read from LDS while
 // the current stage's MFMAs run; one barrier per stage.
 //
-// LDS layout of a stage: row r is 4 chunks of 16 bytes; logical chunk c of
-// row r sits in slot c ^ perm(r), so the 16-byte fragment reads of
-// consecutive rows at the same logical chunk hit distinct banks.  A
-// load-to-LDS instruction writes 64 lanes x 16 bytes contiguously (16 rows);
-// lane l therefore fetches row l / 4 of its group at the logical chunk that
-// belongs in slot l % 4.
+// LDS layout of a stage: rows are paired into 128-byte lines, row r in line
+// r / 2; a line holds 8 chunks of 16 bytes, and logical chunk c of row r
+// (position (r % 2) * 4 + c in its line) sits in slot position ^ (line % 8).
+// A fragment read (16 consecutive rows at one chunk per 16 lanes) then runs
+// at the full LDS read rate of gfx950; plain or row-XOR-swizzled 64-byte rows
+// measure at half of it.  A load-to-LDS instruction writes 64 lanes x 16
+// bytes contiguously (8 lines = 16 rows); lane l fills line l / 8, slot l % 8,
+// and so fetches the row and chunk that the swizzle assigns to that slot.
 #pragma once
 
 #include <type_traits>
@@ -38,6 +40,9 @@ __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 0xF) | (((N >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8));
 }
+
+// s_waitcnt lgkmcnt(0) (vmcnt and expcnt left unconstrained)
+__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt((0xF) | (0x3 << 14) | (0x7 << 4)); }
 
 __device__ __forceinline__ uint32_t lds_address(const void* p) {
   // a generic pointer into LDS converted to the 32-bit LDS byte address
@@ -66,11 +71,17 @@ struct TileMma {
   static_assert(kWTM % 16 == 0 && kWTN % 16 == 0, "wave tile must be 16-aligned");
   static_assert(NS >= 3, "ring depth");
 
-  // chunk slot permutation of row r: the 16-byte reads of 16 consecutive rows
-  // at one logical chunk fall in 16 distinct 16-byte bank groups (and any 8
-  // consecutive rows in 8 distinct groups of a 128-byte window)
-  __device__ __forceinline__ static int perm(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
-  __device__ __forceinline__ static int swz(int r, int c) { return r * kRowBytes + ((c ^ perm(r)) << 4); }
+  // byte offset within a stage of logical chunk c (0..3) of local row r
+  __device__ __forceinline__ static int swz(int r, int c) {
+    const int line = r >> 1;
+    return line * 128 + (((((r & 1) << 2) | c) ^ (line & 7)) << 4);
+  }
+  // (row, chunk) that lane l of load instruction `grp` (rows 16 grp .. 16 grp + 15) fetches
+  __device__ __forceinline__ static int dma_row(int grp, int l) {
+    const int q = l >> 3, s = (l & 7) ^ q;
+    return grp * 16 + 2 * q + (s >> 2);
+  }
+  __device__ __forceinline__ static int dma_chunk(int l) { return ((l & 7) ^ (l >> 3)) & 3; }
 
   // a_off(r) / b_off(r): byte offset of local row r (already clamped to a
   // valid row) relative to A / B.  nk: number of K stages.  smem: kSmem bytes.
@@ -86,15 +97,9 @@ struct TileMma {
     // this lane's source rows/chunks for the wave's load instructions
     uint32_t ga[kIA], gb[kIB];
 #pragma unroll
-    for (int i = 0; i < kIA; ++i) {
-      const int r = (wave * kIA + i) * 16 + (lane >> 2);
-      ga[i] = a_off(r) + (((lane & 3) ^ perm(r)) << 4);
-    }
+    for (int i = 0; i < kIA; ++i) ga[i] = a_off(dma_row(wave * kIA + i, lane)) + (dma_chunk(lane) << 4);
 #pragma unroll
-    for (int i = 0; i < kIB; ++i) {
-      const int r = (wave * kIB + i) * 16 + (lane >> 2);
-      gb[i] = b_off(r) + (((lane & 3) ^ perm(r)) << 4);
-    }
+    for (int i = 0; i < kIB; ++i) gb[i] = b_off(dma_row(wave * kIB + i, lane)) + (dma_chunk(lane) << 4);
     const uint32_t lds0 = lds_address(smem);
     auto issue = [&](int kt, int buf) {
       const uint32_t koff = uint32_t(kt) * kRowBytes;
@@ -131,35 +136,43 @@ struct TileMma {
         for (int n = 0; n < kFN; ++n) Mfma<T>::run(acc[m][n], af[slot][m], bfr[slot][n]);
     };
 
+    // Every step has the same shape: no branch but the loop's back-edge (a
+    // branch inside a step makes the compiler's wait-count analysis wait for
+    // the next stage's fragment reads before the MFMAs of the current one).
+    // Past the last stage the loads repeat stage nk - 1 into the free ring
+    // buffer, so that the number of loads in flight, and with it every vmcnt
+    // wait, stays uniform.  Such a buffer is never read as a live stage: at
+    // step kt it is the buffer of stage kt - 1, and the at most NS - 2 stages
+    // still to be read occupy the buffers of kt + 1 .. kt + NS - 2.
 #pragma unroll
-    for (int s = 0; s < NS - 1; ++s)
-      if (s < nk) issue(s, s);
-    wait_vmcnt<0>();
+    for (int s = 0; s < NS - 1; ++s) issue(min(s, nk - 1), s);
+    wait_vmcnt<(NS - 2) * (kIA + kIB)>();   // stage 0 landed
     __syncthreads();
     read_frags(0, 0);
-    // Iteration kt multiplies stage kt (fragments already in registers) while
-    // the fragments of stage kt + 1 are read.  Its barrier needs stage kt + 1
+    // Step kt multiplies stage kt (fragments already in registers) while the
+    // fragments of stage kt + 1 are read.  Its barrier needs stage kt + 1
     // landed in every wave; it also proves every wave has finished reading
-    // stage kt - 1 (read during iteration kt - 2), so that buffer takes the
-    // load of stage kt + NS - 1.
+    // stage kt - 1 (read during step kt - 2), so that buffer takes the load
+    // of stage kt + NS - 1.  nk is even (checked by the launchers).
+    // Scheduling fences keep each step's fragment reads ahead of its MFMAs
+    // and the MFMAs inside their step; left free, the scheduler pairs every
+    // read with the MFMA that consumes it and undoes the pipelining.
     auto step = [&](int kt, auto cur, auto nxt) {
-      if (kt + 1 < nk) {
-        if (kt + NS - 2 < nk)
-          wait_vmcnt<kInflightNext>();
-        else
-          wait_vmcnt<0>();
-        __syncthreads();
-        if (kt + NS - 1 < nk) issue(kt + NS - 1, (kt + NS - 1) % NS);
-        read_frags(kt + 1, decltype(nxt)::value);
-      }
+      __builtin_amdgcn_sched_barrier(0);
+      wait_vmcnt<kInflightNext>();
+      __syncthreads();
+      issue(min(kt + NS - 1, nk - 1), (kt + NS - 1) % NS);
+      read_frags(kt + 1, decltype(nxt)::value);
+      __builtin_amdgcn_sched_barrier(0);
       mma(decltype(cur)::value);
     };
     using S0 = std::integral_constant<int, 0>;
     using S1 = std::integral_constant<int, 1>;
     for (int kt = 0; kt < nk; kt += 2) {
       step(kt, S0{}, S1{});
-      if (kt + 1 < nk) step(kt + 1, S1{}, S0{});
+      step(kt + 1, S1{}, S0{});
     }
+    wait_vmcnt<0>();
     __syncthreads();   // the caller may reuse the LDS
   }
 };
