@@ -3,21 +3,21 @@
 //
 // A workgroup computes a BM x BN tile with WAVES_M x WAVES_N waves; each wave
 // owns a (BM/WAVES_M) x (BN/WAVES_N) sub-tile made of 16x16 MFMA blocks.
-// K advances in stages of 64 bytes per row (32 bf16 or 16 fp32 values).
-// Stages are copied from global memory straight into a ring of NS LDS
-// buffers with global_load_lds_dwordx4 (no register staging), NS - 1 stages
-// ahead of the stage being multiplied, so a load has NS - 2 stages of MFMA
-// work to land; the MMA fragments of the next stage are read from LDS while
-// the current stage's MFMAs run; one barrier per stage.
+// K advances in stages of 128 bytes per row (64 bf16 or 32 fp32 values),
+// copied from global memory straight into a two-slot LDS ring with
+// global_load_lds_dwordx4 (no register staging); each load instruction
+// moves 8 whole 128-byte rows, i.e. full cache lines.  A stage is consumed
+// in two MFMA sub-steps of 64 bytes of K; the fragments of the next
+// sub-step are read from LDS while the current one's MFMAs run, and one
+// barrier per stage hands the just-consumed slot to the load of the stage
+// after next, so a load has a full stage of MFMA work to land.
 //
-// LDS layout of a stage: rows are paired into 128-byte lines, row r in line
-// r / 2; a line holds 8 chunks of 16 bytes, and logical chunk c of row r
-// (position (r % 2) * 4 + c in its line) sits in slot position ^ (line % 8).
-// A fragment read (16 consecutive rows at one chunk per 16 lanes) then runs
-// at the full LDS read rate of gfx950; plain or row-XOR-swizzled 64-byte rows
-// measure at half of it.  A load-to-LDS instruction writes 64 lanes x 16
-// bytes contiguously (8 lines = 16 rows); lane l fills line l / 8, slot l % 8,
-// and so fetches the row and chunk that the swizzle assigns to that slot.
+// LDS layout of a stage: row r is 128 bytes = 8 chunks of 16 bytes, logical
+// chunk c in slot c ^ (r % 8).  A fragment read (16 consecutive rows at one
+// chunk per 16 lanes) then stays near the full LDS read rate of gfx950.  A
+// load instruction writes 64 lanes x 16 bytes contiguously (8 rows); lane l
+// fills row l / 8, slot l % 8, and so fetches the chunk that the swizzle
+// assigns to that slot.
 #pragma once
 
 #include <type_traits>
@@ -26,12 +26,27 @@
 
 namespace dllm {
 
-// Asynchronous 16-byte copy global -> LDS.  lds_addr is the wave-uniform LDS
-// byte address of the 1 KB block the 64 lanes fill.  Issued through inline
-// assembly so the compiler does not insert a conservative wait for it before
-// every LDS read; completion is awaited explicitly with wait_vmcnt.
-__device__ __forceinline__ void lds_dma16(const void* gptr, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_addr) : "memory", "m0");
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+
+// Raw buffer resource (gfx9 layout: 48-bit base, stride 0, num_records,
+// word 3 = 32-bit data format) for a range starting at p.  num_records is the
+// maximum: every offset used with it is a clamped in-range row offset.
+__device__ __forceinline__ i32x4 buffer_rsrc(const void* p) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  return i32x4{__builtin_amdgcn_readfirstlane(int(uint32_t(a))),
+               __builtin_amdgcn_readfirstlane(int(uint32_t(a >> 32) & 0xFFFF)), -1, 0x00020000};
+}
+
+// Asynchronous 16-byte-per-lane copy buffer -> LDS: lane l reads base +
+// voff + soff and writes LDS byte lds_addr + 16 l, where lds_addr is the
+// wave-uniform LDS address of the 1 KB block the 64 lanes fill.  Issued
+// through inline assembly so the compiler does not insert a conservative
+// wait for it before every LDS read; completion is awaited explicitly with
+// wait_vmcnt.
+__device__ __forceinline__ void lds_dma16(i32x4 rsrc, uint32_t voff, uint32_t soff, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %3\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(voff), "s"(rsrc), "s"(soff),
+               "s"(lds_addr)
+               : "memory", "m0");
 }
 
 // s_waitcnt vmcnt(N) (expcnt and lgkmcnt left unconstrained)
@@ -44,12 +59,21 @@ __device__ __forceinline__ void wait_vmcnt() {
 // s_waitcnt lgkmcnt(0) (vmcnt and expcnt left unconstrained)
 __device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt((0xF) | (0x3 << 14) | (0x7 << 4)); }
 
+// f(integral_constant<int, i>) for i = B .. E - 1, unrolled at compile time
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
 __device__ __forceinline__ uint32_t lds_address(const void* p) {
   // a generic pointer into LDS converted to the 32-bit LDS byte address
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) uint8_t*)(p)));
 }
 
-template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, int NS = 4>
+template <typename T, int BM, int BN, int WAVES_M, int WAVES_N>
 struct TileMma {
   static constexpr int kWaves = WAVES_M * WAVES_N;
   static constexpr int kThreads = kWaves * kWave;
@@ -57,59 +81,55 @@ struct TileMma {
   static constexpr int kWTN = BN / WAVES_N;
   static constexpr int kFM = kWTM / 16;
   static constexpr int kFN = kWTN / 16;
-  static constexpr int kRowBytes = 64;
+  static constexpr int kRowBytes = 128;                    // one stage of one row
   static constexpr int kStageA = BM * kRowBytes;
   static constexpr int kStageB = BN * kRowBytes;
   static constexpr int kStage = kStageA + kStageB;
-  static constexpr int kSmem = NS * kStage;
-  static constexpr int kKPerStage = kRowBytes / Elem<T>::bytes;
-  static constexpr int kIA = BM / 16 / kWaves;   // load-to-LDS instructions per wave per stage (A)
-  static constexpr int kIB = BN / 16 / kWaves;   // (B)
-  // load instructions of later stages allowed in flight while stage kt + 1 must have landed
-  static constexpr int kInflightNext = (NS - 3) * (kIA + kIB);
-  static_assert(kIA * kWaves * 16 == BM && kIB * kWaves * 16 == BN, "tile / wave mismatch");
+  static constexpr int kSmem = 2 * kStage;
+  static constexpr int kKPerStage = 64 / Elem<T>::bytes;   // K of one MFMA sub-step; K must be a multiple of twice this
+  static constexpr int kIA = BM / 8 / kWaves;               // load-to-LDS instructions per wave per stage (A)
+  static constexpr int kIB = BN / 8 / kWaves;               // (B)
+  static_assert(kIA * kWaves * 8 == BM && kIB * kWaves * 8 == BN, "tile / wave mismatch");
   static_assert(kWTM % 16 == 0 && kWTN % 16 == 0, "wave tile must be 16-aligned");
-  static_assert(NS >= 3, "ring depth");
 
-  // byte offset within a stage of logical chunk c (0..3) of local row r
-  __device__ __forceinline__ static int swz(int r, int c) {
-    const int line = r >> 1;
-    return line * 128 + (((((r & 1) << 2) | c) ^ (line & 7)) << 4);
-  }
-  // (row, chunk) that lane l of load instruction `grp` (rows 16 grp .. 16 grp + 15) fetches
-  __device__ __forceinline__ static int dma_row(int grp, int l) {
-    const int q = l >> 3, s = (l & 7) ^ q;
-    return grp * 16 + 2 * q + (s >> 2);
-  }
-  __device__ __forceinline__ static int dma_chunk(int l) { return ((l & 7) ^ (l >> 3)) & 3; }
+  // byte offset within a stage of logical chunk c (0..7) of local row r
+  __device__ __forceinline__ static int swz(int r, int c) { return r * kRowBytes + ((c ^ (r & 7)) << 4); }
 
   // a_off(r) / b_off(r): byte offset of local row r (already clamped to a
-  // valid row) relative to A / B.  nk: number of K stages.  smem: kSmem bytes.
+  // valid row) relative to A / B.  nk: K / kKPerStage (even).  smem: kSmem bytes.
   template <class AOff, class BOff>
   __device__ __forceinline__ static void run(uint8_t* smem, const uint8_t* A, const uint8_t* B, AOff a_off,
                                              BOff b_off, int nk, f32x4 (&acc)[kFM][kFN]) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    // wave index as a scalar: the LDS addresses of the load instructions are
+    // then computed on the scalar unit, with no per-load register round trip
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / WAVES_N;
     const int wn = wave % WAVES_N;
+    const int ns = nk >> 1;   // stages
 
-    // this lane's source rows/chunks for the wave's load instructions
+    // this lane's source row and chunk for each of the wave's load instructions
+    const uint32_t chunk_off = uint32_t((lane & 7) ^ (lane >> 3)) << 4;
     uint32_t ga[kIA], gb[kIB];
 #pragma unroll
-    for (int i = 0; i < kIA; ++i) ga[i] = a_off(dma_row(wave * kIA + i, lane)) + (dma_chunk(lane) << 4);
+    for (int i = 0; i < kIA; ++i) ga[i] = a_off((wave * kIA + i) * 8 + (lane >> 3)) + chunk_off;
 #pragma unroll
-    for (int i = 0; i < kIB; ++i) gb[i] = b_off(dma_row(wave * kIB + i, lane)) + (dma_chunk(lane) << 4);
+    for (int i = 0; i < kIB; ++i) gb[i] = b_off((wave * kIB + i) * 8 + (lane >> 3)) + chunk_off;
     const uint32_t lds0 = lds_address(smem);
-    auto issue = [&](int kt, int buf) {
-      const uint32_t koff = uint32_t(kt) * kRowBytes;
-      const uint32_t sbase = lds0 + buf * kStage;
+    const i32x4 ra = buffer_rsrc(A), rb = buffer_rsrc(B);
+    auto dma_a = [&](int i, uint32_t koff, uint32_t sbase) {
+      lds_dma16(ra, ga[i], koff, sbase + (wave * kIA + i) * 1024);
+    };
+    auto dma_b = [&](int i, uint32_t koff, uint32_t sbase) {
+      lds_dma16(rb, gb[i], koff, sbase + kStageA + (wave * kIB + i) * 1024);
+    };
+    auto issue = [&](int st, int slot) {
+      const uint32_t koff = uint32_t(st) * kRowBytes, sbase = lds0 + slot * kStage;
 #pragma unroll
-      for (int i = 0; i < kIA; ++i)
-        lds_dma16(A + ga[i] + koff, __builtin_amdgcn_readfirstlane(sbase + (wave * kIA + i) * 1024));
+      for (int i = 0; i < kIA; ++i) dma_a(i, koff, sbase);
 #pragma unroll
-      for (int i = 0; i < kIB; ++i)
-        lds_dma16(B + gb[i] + koff, __builtin_amdgcn_readfirstlane(sbase + kStageA + (wave * kIB + i) * 1024));
+      for (int i = 0; i < kIB; ++i) dma_b(i, koff, sbase);
     };
 
 #pragma unroll
@@ -119,58 +139,92 @@ struct TileMma {
 
     const int fr = lane & 15;
     const int fc = lane >> 4;
-    u32x4 af[2][kFM], bfr[2][kFN];   // fragments of the current and the next stage
-    auto read_frags = [&](int kt, int slot) {
-      const uint8_t* s = smem + (kt % NS) * kStage;
-#pragma unroll
-      for (int m = 0; m < kFM; ++m)
-        af[slot][m] = *reinterpret_cast<const u32x4*>(s + swz(wm * kWTM + m * 16 + fr, fc));
-#pragma unroll
-      for (int n = 0; n < kFN; ++n)
-        bfr[slot][n] = *reinterpret_cast<const u32x4*>(s + kStageA + swz(wn * kWTN + n * 16 + fr, fc));
+    u32x4 af[2][kFM], bfr[2][kFN];   // fragments of the current and the next sub-step
+    // fragments of sub-step h (0 or 1) of the stage in LDS slot `slot`
+    auto a_frag = [&](int slot, int h, int m) {
+      return *reinterpret_cast<const u32x4*>(smem + slot * kStage + swz(wm * kWTM + m * 16 + fr, 4 * h + fc));
     };
-    auto mma = [&](int slot) {
-#pragma unroll
-      for (int m = 0; m < kFM; ++m)
-#pragma unroll
-        for (int n = 0; n < kFN; ++n) Mfma<T>::run(acc[m][n], af[slot][m], bfr[slot][n]);
+    auto b_frag = [&](int slot, int h, int n) {
+      return *reinterpret_cast<const u32x4*>(smem + slot * kStage + kStageA +
+                                             swz(wn * kWTN + n * 16 + fr, 4 * h + fc));
+    };
+    auto mma_one = [&](int r, int i) {
+      Mfma<T>::run(acc[i / kFN][i % kFN], af[r][i / kFN], bfr[r][i % kFN]);
     };
 
     // Every step has the same shape: no branch but the loop's back-edge (a
     // branch inside a step makes the compiler's wait-count analysis wait for
-    // the next stage's fragment reads before the MFMAs of the current one).
-    // Past the last stage the loads repeat stage nk - 1 into the free ring
-    // buffer, so that the number of loads in flight, and with it every vmcnt
-    // wait, stays uniform.  Such a buffer is never read as a live stage: at
-    // step kt it is the buffer of stage kt - 1, and the at most NS - 2 stages
-    // still to be read occupy the buffers of kt + 1 .. kt + NS - 2.
-#pragma unroll
-    for (int s = 0; s < NS - 1; ++s) issue(min(s, nk - 1), s);
-    wait_vmcnt<(NS - 2) * (kIA + kIB)>();   // stage 0 landed
+    // the next fragment reads before the current MFMAs).  Past the last stage
+    // the loads repeat stage ns - 1 into the slot just released, so that the
+    // number of loads in flight, and with it every vmcnt wait, stays uniform;
+    // that slot is not read again as a live stage.
+    issue(0, 0);
+    issue(min(1, ns - 1), 1);
+    wait_vmcnt<kIA + kIB>();   // stage 0 landed
     __syncthreads();
-    read_frags(0, 0);
-    // Step kt multiplies stage kt (fragments already in registers) while the
-    // fragments of stage kt + 1 are read.  Its barrier needs stage kt + 1
-    // landed in every wave; it also proves every wave has finished reading
-    // stage kt - 1 (read during step kt - 2), so that buffer takes the load
-    // of stage kt + NS - 1.  nk is even (checked by the launchers).
-    // Scheduling fences keep each step's fragment reads ahead of its MFMAs
-    // and the MFMAs inside their step; left free, the scheduler pairs every
-    // read with the MFMA that consumes it and undoes the pipelining.
-    auto step = [&](int kt, auto cur, auto nxt) {
-      __builtin_amdgcn_sched_barrier(0);
-      wait_vmcnt<kInflightNext>();
-      __syncthreads();
-      issue(min(kt + NS - 1, nk - 1), (kt + NS - 1) % NS);
-      read_frags(kt + 1, decltype(nxt)::value);
-      __builtin_amdgcn_sched_barrier(0);
-      mma(decltype(cur)::value);
+#pragma unroll
+    for (int m = 0; m < kFM; ++m) af[0][m] = a_frag(0, 0, m);
+#pragma unroll
+    for (int n = 0; n < kFN; ++n) bfr[0][n] = b_frag(0, 0, n);
+
+    // Sub-step 0 of stage j: MFMAs on the fragments of (j, 0) (register set
+    // 0) with the reads of (j, 1) into set 1 spread between them.
+    // Sub-step 1: the MFMAs on (j, 1) that need nothing from this step go
+    // before the barrier; the barrier needs stage j + 1 landed in every wave
+    // and proves every wave has read its last fragments of stage j, so the
+    // slot of j takes the load of stage j + 2; after it, each remaining MFMA
+    // is followed by one load instruction or one read of (j + 1, 0) into set
+    // 0.  Scheduling fences pin this order (left free, the scheduler pairs
+    // every fragment read with the MFMA that consumes it).
+    constexpr int kMma = kFM * kFN;
+    constexpr int kReads = kFM + kFN;
+    constexpr int kStride0 = kMma / kReads > 0 ? kMma / kReads : 1;
+    constexpr int kComp1 = kIA + kIB + kReads;
+    constexpr int kPre1 = kMma > kComp1 ? kMma - kComp1 : 0;
+    auto read_into = [&](int r, int slot, int h, int j) {   // j-th fragment read of a sub-step
+      if (j < kFM)
+        af[r][j] = a_frag(slot, h, j);
+      else
+        bfr[r][j - kFM] = b_frag(slot, h, j - kFM);
     };
-    using S0 = std::integral_constant<int, 0>;
-    using S1 = std::integral_constant<int, 1>;
-    for (int kt = 0; kt < nk; kt += 2) {
-      step(kt, S0{}, S1{});
-      step(kt + 1, S1{}, S0{});
+    for (int j = 0; j < ns; ++j) {
+      const int cur = j & 1, nxt = cur ^ 1;
+      __builtin_amdgcn_sched_barrier(0);
+      static_for<0, kMma>([&](auto ii) {
+        constexpr int i = decltype(ii)::value;
+        mma_one(0, i);
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (i % kStride0 == kStride0 - 1 && i / kStride0 < kReads) {
+          read_into(1, cur, 1, i / kStride0);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      });
+      static_for<kMma / kStride0, kReads>([&](auto jj) {   // reads left over when kMma < kReads
+        read_into(1, cur, 1, decltype(jj)::value);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      static_for<0, kPre1>([&](auto ii) {
+        mma_one(1, decltype(ii)::value);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      wait_vmcnt<0>();
+      __syncthreads();
+      __builtin_amdgcn_sched_barrier(0);
+      const uint32_t koff = uint32_t(min(j + 2, ns - 1)) * kRowBytes, sbase = lds0 + cur * kStage;
+      static_for<0, kComp1>([&](auto cc) {
+        constexpr int c = decltype(cc)::value;
+        if constexpr (kPre1 + c < kMma) {
+          mma_one(1, kPre1 + c);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        if constexpr (c < kIA)
+          dma_a(c, koff, sbase);
+        else if constexpr (c < kIA + kIB)
+          dma_b(c - kIA, koff, sbase);
+        else
+          read_into(0, nxt, 0, c - kIA - kIB);
+        __builtin_amdgcn_sched_barrier(0);
+      });
     }
     wait_vmcnt<0>();
     __syncthreads();   // the caller may reuse the LDS
