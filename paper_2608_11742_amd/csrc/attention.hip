@@ -3,8 +3,9 @@
 // (shared by all sequences of the batch).
 //
 // A workgroup of 4 waves takes 128 queries of one (sequence, head); each
-// wave owns 32 queries.  Keys stream through LDS in tiles of 64 (K rows and
-// V^T columns, double-buffered, next tile prefetched into registers).
+// wave owns 32 queries, two workgroups share a CU.  Keys stream through a
+// two-slot LDS ring in tiles of 64 (K rows and V^T columns), copied from
+// global memory straight into LDS with buffer_load ... lds one tile ahead.
 // Scores are computed transposed, S^T = K Q^T, so in the MFMA output layout
 // every lane holds one query's scores for 4 keys per 16-key block: the
 // online-softmax max/sum and the output rescale stay per lane, and the
@@ -12,6 +13,7 @@
 // MFMA operands without an LDS round trip.
 #include "kernels.h"
 #include "common.h"
+#include "mainloop.h"
 
 namespace dllm {
 
@@ -31,31 +33,43 @@ struct AttnCfg {
   static constexpr int KB = kKT * CK * 16;                 // K tile bytes
   static constexpr int VB = HD * CV * 16;                  // V^T tile bytes
   static constexpr int STAGE = KB + VB;
-  static constexpr int KLD = kKT * CK / kThreads;          // K chunks per thread
-  static constexpr int VLD = HD * CV / kThreads;           // V chunks per thread
+  static constexpr int RK = 64 / CK;                       // K rows per load instruction (1 KB)
+  static constexpr int RV = 64 / CV;                       // V^T rows per load instruction
+  static constexpr int IK = kKT * CK / 64 / kWaves;        // K load instructions per wave per tile
+  static constexpr int IV = HD * CV / 64 / kWaves;         // V^T load instructions per wave per tile
   static constexpr int NDB = HD / 16;                      // 16-row dim blocks of O^T
   static constexpr int QSTEPS = CK / 4;                    // MFMA k-steps over head_dim
-  static_assert(KLD * kThreads == kKT * CK && VLD * kThreads == HD * CV, "tile split");
+  static_assert(CK >= 8 && CV >= 8, "rows of at least 8 chunks (swizzle)");
+  static_assert(IK * kWaves * 64 == kKT * CK && IV * kWaves * 64 == HD * CV, "tile split");
 };
 
+// row r, chunk c of a tile stored with rows of `row_bytes`: chunk slot c ^ (r % 8)
 __device__ __forceinline__ int swz(int r, int c, int row_bytes) { return r * row_bytes + ((c ^ (r & 7)) << 4); }
 
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t v = {static_cast<__bf16>(a), static_cast<__bf16>(b)};   // round to nearest even
+  return __builtin_bit_cast(uint32_t, v);
+}
+
 template <typename T, int HD>
-__global__ __launch_bounds__(kThreads, (HD * Elem<T>::bytes >= 256 ? 1 : 2)) void attn_kernel(AttnArgs a,
-                                                                                              float qk_scale_log2) {
+__global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_scale_log2) {
   using C = AttnCfg<T, HD>;
   __shared__ __attribute__((aligned(16))) uint8_t smem[2 * C::STAGE];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int fr = lane & 15, g = lane >> 4;
   const int b = blockIdx.z, h = blockIdx.y;
   const int q0 = blockIdx.x * kQT + wave * kQW;
   const size_t bh = size_t(b) * a.H + h;
 
   const T* Q = static_cast<const T*>(a.q) + bh * a.Sq * HD;
-  const T* Ko = static_cast<const T*>(a.k) + bh * a.Sq * HD;
-  const T* Vo = static_cast<const T*>(a.vt) + bh * HD * a.vt_ld;
-  const T* Kp = a.kp ? static_cast<const T*>(a.kp) + size_t(h) * a.p_cap * HD : nullptr;
-  const T* Vp = a.kp ? static_cast<const T*>(a.vpt) + size_t(h) * HD * a.p_cap : nullptr;
+  const uint8_t* Ko = reinterpret_cast<const uint8_t*>(static_cast<const T*>(a.k) + bh * a.Sq * HD);
+  const uint8_t* Vo = reinterpret_cast<const uint8_t*>(static_cast<const T*>(a.vt) + bh * HD * a.vt_ld);
+  const uint8_t* Kp = a.kp ? reinterpret_cast<const uint8_t*>(static_cast<const T*>(a.kp) + size_t(h) * a.p_cap * HD)
+                           : nullptr;
+  const uint8_t* Vp =
+      a.kp ? reinterpret_cast<const uint8_t*>(static_cast<const T*>(a.vpt) + size_t(h) * HD * a.p_cap) : nullptr;
   const int n_pt = a.kp ? cdiv(a.p_len, kKT) : 0;
   const int n_ot = cdiv(a.Sq, kKT);
   const int n_tiles = n_pt + n_ot;
@@ -71,88 +85,84 @@ __global__ __launch_bounds__(kThreads, (HD * Elem<T>::bytes >= 256 ? 1 : 2)) voi
                                                    (4 * st + g) * 16);
   }
 
-  // global -> register prefetch of one key tile, K and V^T halves separately
-  // (the K half is live during QK^T, the V half during PV)
-  u32x4 rk[C::KLD], rv[C::VLD];
-  auto gload_k = [&](int t) {
-    const bool pre = t < n_pt;
-    const int k0 = (pre ? t : t - n_pt) * kKT;
-    const int nk = pre ? a.p_len : a.Sq;
-    const T* Kb = pre ? Kp : Ko;
+  const uint32_t lds0 = lds_address(smem);
+  // key range of tile t: source, first key, number of valid keys of the source, V^T row pitch
+  struct Src {
+    const uint8_t* k;
+    const uint8_t* v;
+    int k0, nk, ld;
+  };
+  auto src = [&](int t) -> Src {
+    if (t < n_pt) return Src{Kp, Vp, t * kKT, a.p_len, a.p_cap};
+    return Src{Ko, Vo, (t - n_pt) * kKT, a.Sq, a.vt_ld};
+  };
+  // Copy tile t into ring slot `slot`.  Lane l of a load instruction fills
+  // row l / C, slot l % C of its block and fetches the chunk the swizzle
+  // assigns there.  Rows past the last valid key read the last valid row and
+  // V^T chunks past the row pitch read the row's last chunk: every address
+  // stays inside the source, and those keys are masked (K) or zeroed (V^T).
+  auto issue = [&](int t, int slot) {
+    const Src s = src(t);
+    const i32x4 rk = buffer_rsrc(s.k), rv = buffer_rsrc(s.v);
+    const uint32_t base = lds0 + slot * C::STAGE;
 #pragma unroll
-    for (int i = 0; i < C::KLD; ++i) {
-      const int qd = tid + kThreads * i, r = qd / C::CK, c = qd % C::CK;
-      const int key = min(k0 + r, nk - 1);
-      rk[i] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint8_t*>(Kb + size_t(key) * HD) + c * 16);
+    for (int i = 0; i < C::IK; ++i) {
+      const int grp = wave * C::IK + i;
+      const int r = grp * C::RK + lane / C::CK, c = (lane % C::CK) ^ (r & 7);
+      const int key = min(s.k0 + r, s.nk - 1);
+      lds_dma16(rk, uint32_t(key) * (HD * Elem<T>::bytes) + c * 16, 0, base + grp * 1024);
+    }
+#pragma unroll
+    for (int i = 0; i < C::IV; ++i) {
+      const int grp = wave * C::IV + i;
+      const int r = grp * C::RV + lane / C::CV, c = (lane % C::CV) ^ (r & 7);
+      const int key = min(s.k0 + c * C::E, s.ld - C::E);
+      lds_dma16(rv, (uint32_t(r) * s.ld + key) * Elem<T>::bytes, 0, base + C::KB + grp * 1024);
     }
   };
-  auto gload_v = [&](int t) {
-    const bool pre = t < n_pt;
-    const int k0 = (pre ? t : t - n_pt) * kKT;
-    const int nk = pre ? a.p_len : a.Sq;
-    const T* Vb = pre ? Vp : Vo;
-    const int ld = pre ? a.p_cap : a.vt_ld;
-#pragma unroll
-    for (int i = 0; i < C::VLD; ++i) {
-      const int qd = tid + kThreads * i, r = qd / C::CV, c = qd % C::CV;
-      const int key0 = k0 + c * C::E;
-      u32x4 v = u32x4{0u, 0u, 0u, 0u};
-      if (key0 < nk) {
-        v = *reinterpret_cast<const u32x4*>(Vb + size_t(r) * ld + key0);
-        if (key0 + C::E > nk) {   // ragged tail: zero the values of keys >= nk
-          const int valid = nk - key0;
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            const int e_lo = w * (C::E / 4);
-            if constexpr (C::E == 8) {
-              uint32_t m = (e_lo < valid ? 0xffffu : 0u) | (e_lo + 1 < valid ? 0xffff0000u : 0u);
-              v[w] &= m;
-            } else {
-              if (e_lo >= valid) v[w] = 0u;
-            }
-          }
-        }
+  auto ragged = [&](int t) {
+    const Src s = src(t);
+    return s.nk - s.k0 < kKT;
+  };
+  // zero the V^T values of keys >= nk in a ragged tile (after it has landed)
+  auto zero_tail = [&](int t, int slot) {
+    const Src s = src(t);
+    const int valid = s.nk - s.k0;
+    uint8_t* sv = smem + slot * C::STAGE + C::KB;
+    for (int q = tid; q < HD * C::CV; q += kThreads) {
+      const int r = q / C::CV, c = q % C::CV, e0 = c * C::E;
+      if (e0 + C::E <= valid) continue;
+      u32x4* p = reinterpret_cast<u32x4*>(sv + swz(r, c, C::CV * 16));
+      if (e0 >= valid) {
+        *p = u32x4{0u, 0u, 0u, 0u};
+      } else {
+        T* el = reinterpret_cast<T*>(p);
+        for (int e = valid - e0; e < C::E; ++e) el[e] = T{};
       }
-      rv[i] = v;
-    }
-  };
-  auto sstore_k = [&](int buf) {
-    uint8_t* s = smem + buf * C::STAGE;
-#pragma unroll
-    for (int i = 0; i < C::KLD; ++i) {
-      const int qd = tid + kThreads * i, r = qd / C::CK, c = qd % C::CK;
-      *reinterpret_cast<u32x4*>(s + swz(r, c, C::CK * 16)) = rk[i];
-    }
-  };
-  auto sstore_v = [&](int buf) {
-    uint8_t* s = smem + buf * C::STAGE;
-#pragma unroll
-    for (int i = 0; i < C::VLD; ++i) {
-      const int qd = tid + kThreads * i, r = qd / C::CV, c = qd % C::CV;
-      *reinterpret_cast<u32x4*>(s + C::KB + swz(r, c, C::CV * 16)) = rv[i];
     }
   };
 
   f32x4 o[C::NDB][2];
 #pragma unroll
   for (int db = 0; db < C::NDB; ++db) o[db][0] = o[db][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float mrun[2] = {-INFINITY, -INFINITY};
+  float mrun[2] = {-INFINITY, -INFINITY};   // running max of the scaled scores (exp2 domain)
   float lrun[2] = {0.f, 0.f};
 
-  gload_k(0);
-  gload_v(0);
-  sstore_k(0);
-  sstore_v(0);
+  issue(0, 0);
+  wait_vmcnt<0>();
   __syncthreads();
+  if (ragged(0)) {
+    zero_tail(0, 0);
+    __syncthreads();
+  }
   for (int t = 0; t < n_tiles; ++t) {
     const bool more = t + 1 < n_tiles;
-    if (more) gload_k(t + 1);
+    if (more) issue(t + 1, (t + 1) & 1);   // that slot was last read before the previous barrier
     const uint8_t* s = smem + (t & 1) * C::STAGE;
-    const bool pre = t < n_pt;
-    const int nk = pre ? a.p_len : a.Sq;
-    const int k0 = (pre ? t : t - n_pt) * kKT;
-
     const uint8_t* sv = s + C::KB;
+    const Src sr = src(t);
+    const int k0 = sr.k0, nk = sr.nk;
+
     // the tile's 64 keys in two halves of 32: S^T, online softmax and P V per half
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
@@ -169,12 +179,10 @@ __global__ __launch_bounds__(kThreads, (HD * Elem<T>::bytes >= 256 ? 1 : 2)) voi
           Mfma<T>::run(sc[kk][1], kf, qf[1][st]);
         }
       }
-      if (half == 1 && more) {
-        sstore_k((t + 1) & 1);   // the other buffer's K half was last read before the previous barrier
-        gload_v(t + 1);
-      }
       // online softmax per query column (this lane's query q0 + 16 qb + fr)
       float p[2][2][4];
+      float alpha[2];
+      const bool full = k0 + 32 * half + 32 <= nk;   // every key of this half is valid
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
         float mt = -INFINITY;
@@ -183,42 +191,49 @@ __global__ __launch_bounds__(kThreads, (HD * Elem<T>::bytes >= 256 ? 1 : 2)) voi
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int key = k0 + (2 * half + kk) * 16 + 4 * g + i;
-            const float v = key < nk ? sc[kk][qb][i] * qk_scale_log2 : -INFINITY;
+            const float v = (full || key < nk) ? sc[kk][qb][i] : -INFINITY;
             p[kk][qb][i] = v;
             mt = fmaxf(mt, v);
           }
         mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
         mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-        const float mnew = fmaxf(mrun[qb], mt);
-        const float alpha = __builtin_amdgcn_exp2f(mrun[qb] - mnew);
+        const float mnew = fmaxf(mrun[qb], mt * qk_scale_log2);
+        alpha[qb] = __builtin_amdgcn_exp2f(mrun[qb] - mnew);
         mrun[qb] = mnew;
         float ls = 0.f;
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const float e = __builtin_amdgcn_exp2f(p[kk][qb][i] - mnew);
+            const float e = __builtin_amdgcn_exp2f(fmaf(p[kk][qb][i], qk_scale_log2, -mnew));
             p[kk][qb][i] = e;
             ls += e;
           }
-        lrun[qb] = lrun[qb] * alpha + ls;
+        lrun[qb] = lrun[qb] * alpha[qb] + ls;
+      }
+      // rescale the accumulators only when some query of the wave has a new maximum
+      if (__any(alpha[0] != 1.f || alpha[1] != 1.f)) {
 #pragma unroll
-        for (int db = 0; db < C::NDB; ++db) o[db][qb] *= alpha;
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+          for (int db = 0; db < C::NDB; ++db) o[db][qb] *= alpha[qb];
       }
       // O^T += V^T P^T over keys 32 half .. 32 half + 31
       if constexpr (Elem<T>::per_chunk == 8) {
         // P enters the product as a pair of bf16 values, hi = bf16(p) and
-        // lo = bf16(p - hi), so the weights keep about 16 significant bits.
-        u32x4 ph[2], pl[2];
+        // lo = bf16(p - hi) (both rounded to nearest even), so the weights keep
+        // about 16 significant bits: bf16 weights alone add an error as large as
+        // the bf16 rounding of the output over a thousand keys.
+        u32x4 pb[2], pl[2];
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
           for (int w = 0; w < 4; ++w) {
             const int kk = w >> 1, i0 = 2 * (w & 1);
             const float a0 = p[kk][qb][i0], a1 = p[kk][qb][i0 + 1];
-            const uint16_t h0 = f2bf(a0), h1 = f2bf(a1);
-            ph[qb][w] = uint32_t(h0) | (uint32_t(h1) << 16);
-            pl[qb][w] = uint32_t(f2bf(a0 - bf2f(h0))) | (uint32_t(f2bf(a1 - bf2f(h1))) << 16);
+            const uint32_t hh = pack_bf16x2(a0, a1);
+            pb[qb][w] = hh;
+            pl[qb][w] = pack_bf16x2(a0 - __uint_as_float(hh << 16), a1 - __uint_as_float(hh & 0xffff0000u));
           }
 #pragma unroll
         for (int db = 0; db < C::NDB; ++db) {
@@ -229,7 +244,7 @@ __global__ __launch_bounds__(kThreads, (HD * Elem<T>::bytes >= 256 ? 1 : 2)) voi
           const u32x4 vf = u32x4{lo[0], lo[1], hi[0], hi[1]};
 #pragma unroll
           for (int qb = 0; qb < 2; ++qb) {
-            Mfma<T>::run(o[db][qb], vf, ph[qb]);
+            Mfma<T>::run(o[db][qb], vf, pb[qb]);
             Mfma<T>::run(o[db][qb], vf, pl[qb]);
           }
         }
@@ -252,8 +267,12 @@ __global__ __launch_bounds__(kThreads, (HD * Elem<T>::bytes >= 256 ? 1 : 2)) voi
         }
       }
     }
-    if (more) sstore_v((t + 1) & 1);
+    wait_vmcnt<0>();
     __syncthreads();
+    if (more && ragged(t + 1)) {
+      zero_tail(t + 1, (t + 1) & 1);
+      __syncthreads();
+    }
   }
 
   // normalise and store O[b * Sq + q][h * HD + dim]
@@ -275,6 +294,8 @@ __global__ __launch_bounds__(kThreads, (HD * Elem<T>::bytes >= 256 ? 1 : 2)) voi
 
 template <typename T, int HD>
 hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
+  // the V^T copies read whole 16-byte chunks inside each row of pitch vt_ld / p_cap
+  if (a.vt_ld < 8 || a.vt_ld % 8 || (a.kp && (a.p_cap < 8 || a.p_cap % 8))) return hipErrorInvalidValue;
   const float scale = 1.4426950408889634f / sqrtf(float(HD));
   hipLaunchKernelGGL((attn_kernel<T, HD>), dim3(cdiv(a.Sq, kQT), a.H, a.B), dim3(kThreads), 0, s, a, scale);
   return hipGetLastError();
