@@ -21,15 +21,31 @@ namespace dllm {
 
 namespace {
 
-constexpr int kRows = 128, kCols = 256;
+constexpr int kCols = 256;                               // vocabulary tile
 constexpr int kThreads = 512;
 constexpr int kK = DLLM_TOPK_REG;
-constexpr int kSegs = 4;                                 // threads per row
-constexpr int kSegCols = kCols / kSegs;                  // 64 logits per thread per tile
+constexpr int kSegCols = 64;                             // logits per scan thread per pass
 constexpr int kSegStride = kSegCols * 4 + 16;            // padded segment bytes
-constexpr int kRowStride = kSegs * kSegStride + 16;      // padded row bytes
-constexpr int kStageBytes = kRows * kRowStride;
 constexpr int kTargetWg = 512;
+
+// BM rows per workgroup: 256 (8 waves of 64 x 128, the projection GEMMs'
+// tile) when there are more than 128 rows, else 128 (8 waves of 64 x 64).
+// kSegs scan threads per row, each scanning 64 logits per pass; a pass
+// stages kSegs * 64 columns of the fp32 logit tile in LDS.
+template <typename T, int BM>
+struct LmCfg {
+  using TM = TileMma<T, BM, kCols, BM == 256 ? 4 : 2, BM == 256 ? 2 : 4>;
+  static constexpr int kSegs = kThreads / BM;
+  static constexpr int kPassCols = kSegs * kSegCols;
+  static constexpr int kPasses = kCols / kPassCols;
+  static constexpr int kRowStride = kSegs * kSegStride + 16;   // padded row bytes
+  static constexpr int kStageBytes = BM * kRowStride;
+  static constexpr int kSmem = TM::kSmem > kStageBytes ? TM::kSmem : kStageBytes;
+  static constexpr int kBoundRank = kK / kSegs - 1;            // see the pruning bound below
+  static_assert(kPasses == 1 || kPassCols == TM::kWTN, "a pass is the whole tile or one wave column");
+};
+
+int tile_rows(int R) { return R > 128 ? 256 : 128; }
 
 struct Partials {
   float* m;
@@ -55,16 +71,17 @@ __device__ __forceinline__ void topk_insert(float (&tv)[kK], int (&ti)[kK], floa
   }
 }
 
-template <typename T>
-__global__ __launch_bounds__(kThreads, 2) void lmhead_kernel(const T* __restrict__ Hs, const T* __restrict__ W, int R,
+template <typename T, int BM>
+__global__ __launch_bounds__(kThreads, 1) void lmhead_kernel(const T* __restrict__ Hs, const T* __restrict__ W, int R,
                                                              int d, int V, const float* __restrict__ row_scale,
                                                              const int32_t* __restrict__ rs_idx, int rs_n, int rs_lim,
                                                              float scale, int mask_id, int row_tiles,
                                                              int n_slices,
                                                              int vtiles, Partials part) {
-  using TM = TileMma<T, kRows, kCols, 2, 4>;
-  constexpr int kSmem = TM::kSmem > kStageBytes ? TM::kSmem : kStageBytes;
-  __shared__ __attribute__((aligned(16))) uint8_t smem[kSmem];
+  using Cfg = LmCfg<T, BM>;
+  using TM = typename Cfg::TM;
+  constexpr int kSegs = Cfg::kSegs, kRowStride = Cfg::kRowStride;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[Cfg::kSmem];
 
   // XCD-contiguous ids; all row tiles of one vocabulary slice run on one XCD
   const int nwg = gridDim.x, id = blockIdx.x;
@@ -73,62 +90,122 @@ __global__ __launch_bounds__(kThreads, 2) void lmhead_kernel(const T* __restrict
   const int slice = lin / row_tiles, rt = lin % row_tiles;
   const int t_begin = int((long long)slice * vtiles / n_slices);
   const int t_end = int((long long)(slice + 1) * vtiles / n_slices);
-  const int m0 = rt * kRows;
+  const int m0 = rt * BM;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / 4, wn = wave % 4;
-  // scan role: row tid / 4, segment tid % 4
-  const int srow = tid >> 2, sseg = tid & 3;
+  constexpr int kWavesN = kCols / TM::kWTN;
+  const int wm = wave / kWavesN, wn = wave % kWavesN;
+  // scan role: row tid / kSegs, segment tid % kSegs
+  const int srow = tid / kSegs, sseg = tid % kSegs;
   float m = -INFINITY, s = 0.f, t = 0.f;
+  // This thread's sorted top 16.  With 256-row tiles the mainloop needs
+  // nearly every register, so between tiles the list lives in the thread's
+  // partials slot of the workspace (loaded before the scan, stored after it);
+  // with 128-row tiles it stays in registers.
+  constexpr bool kListInMemory = BM == 256;
+  const int row = m0 + srow;
+  const bool own_row = row < R;   // rows past R scan clamped copies and are discarded
+  size_t slot = size_t(min(row, R - 1)) * part.P + size_t(slice) * kSegs + sseg;
   float tv[kK];
   int ti[kK];
 #pragma unroll
   for (int k = 0; k < kK; ++k) { tv[k] = -INFINITY; ti[k] = 0x7fffffff; }
+  // Pruning bound of the row, shared by its kSegs scan threads: the worst
+  // (by value, then id) of their (16 / kSegs)-th best entries.  Each thread
+  // holds 16 / kSegs entries at least as good as that, so at least 16
+  // entries of the row are at least as good as the bound, and a logit that
+  // is not strictly better cannot reach the row's top 16.  It rises about as
+  // fast as the row's 16th best over all its segments, kSegs times faster
+  // than a thread's own 16th best, which keeps the (wave-divergent)
+  // insertions rare.
+  float bv = -INFINITY;
+  int bi = 0x7fffffff;
 
-  // per-row logit scale of the rows this lane writes in the MFMA layout
-  float rs[TM::kFM][4];
+  // logit scale of this thread's scan row
+  const int srow_c = min(row, R - 1);
+  auto row_logit_scale = [&]() {
+    return scale *
+           (row_scale ? row_scale[rs_idx ? min(max(rs_idx[srow_c % rs_n], 0), rs_lim - 1) : srow_c % rs_n] : 1.0f);
+  };
+  float rs_row = row_logit_scale();
+
+  // the bound from the kSegs threads of this row (consecutive lanes)
+  auto refresh_bound = [&]() {
+    float v = tv[Cfg::kBoundRank];
+    int i = ti[Cfg::kBoundRank];
 #pragma unroll
-  for (int mi = 0; mi < TM::kFM; ++mi)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = min(m0 + wm * TM::kWTM + mi * 16 + 4 * (lane >> 4) + i, R - 1);
-      rs[mi][i] = scale * (row_scale ? row_scale[rs_idx ? min(max(rs_idx[row % rs_n], 0), rs_lim - 1) : row % rs_n] : 1.0f);
+    for (int x = 1; x < kSegs; x <<= 1) {
+      const float ov = __shfl_xor(v, x, 64);
+      const int oi = __shfl_xor(i, x, 64);
+      if (better(v, i, ov, oi)) { v = ov; i = oi; }
     }
+    bv = v;
+    bi = i;
+  };
 
   const uint32_t row_bytes = uint32_t(d) * sizeof(T);
   for (int vt = t_begin; vt < t_end; ++vt) {
+    // opaque per tile: keeps the compiler from hoisting the slot addresses
+    // out of the tile loop, where they would stay live across the mainloop
+    if constexpr (kListInMemory) asm volatile("" : "+v"(slot));
     const int n0 = vt * kCols;
     auto a_off = [&](int r) -> uint32_t { return uint32_t(min(m0 + r, R - 1)) * row_bytes; };
     auto b_off = [&](int r) -> uint32_t { return uint32_t(min(n0 + r, V - 1)) * row_bytes; };
     f32x4 acc[TM::kFM][TM::kFN];
     TM::run(smem, reinterpret_cast<const uint8_t*>(Hs), reinterpret_cast<const uint8_t*>(W), a_off, b_off,
             d / TM::kKPerStage, acc);
-    // stage scaled logits: LDS row r, column c at r * kRowStride + (c / 64) * kSegStride + (c % 64) * 4
+    if constexpr (kListInMemory) {
+      if (vt > t_begin && own_row) {
+        m = part.m[slot];
+        s = part.s[slot];
+        t = part.t[slot];
 #pragma unroll
-    for (int mi = 0; mi < TM::kFM; ++mi)
-#pragma unroll
-      for (int ni = 0; ni < TM::kFN; ++ni)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int r = wm * TM::kWTM + mi * 16 + 4 * (lane >> 4) + i;
-          const int c = wn * TM::kWTN + ni * 16 + (lane & 15);
-          *reinterpret_cast<float*>(smem + r * kRowStride + (c >> 6) * kSegStride + (c & 63) * 4) =
-              acc[mi][ni][i] * rs[mi][i];
+        for (int k = 0; k < kK; ++k) {
+          tv[k] = part.tv[slot * kK + k];
+          ti[k] = part.ti[slot * kK + k];
         }
+      } else {
+        m = -INFINITY;
+        s = t = 0.f;
+#pragma unroll
+        for (int k = 0; k < kK; ++k) { tv[k] = -INFINITY; ti[k] = 0x7fffffff; }
+      }
+      refresh_bound();
+      rs_row = row_logit_scale();
+    }
+#pragma unroll
+    for (int pass = 0; pass < Cfg::kPasses; ++pass) {
+    // stage this pass's scaled logits: LDS row r, pass column c at
+    // r * kRowStride + (c / 64) * kSegStride + (c % 64) * 4
+    if (Cfg::kPasses == 1 || wn == pass) {
+#pragma unroll
+      for (int mi = 0; mi < TM::kFM; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < TM::kFN; ++ni)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int r = wm * TM::kWTM + mi * 16 + 4 * (lane >> 4) + i;
+            const int c = wn * TM::kWTN + ni * 16 + (lane & 15) - pass * Cfg::kPassCols;
+            *reinterpret_cast<float*>(smem + r * kRowStride + (c >> 6) * kSegStride + (c & 63) * 4) = acc[mi][ni][i];
+          }
+    }
     __syncthreads();
-    // scan 64 logits of row srow
+    // scan 64 logits of row srow: running statistics, and a bit mask of the
+    // logits that beat the pruning bound (candidates for the top 16)
     const uint8_t* base = smem + srow * kRowStride + sseg * kSegStride;
-    const int c0 = n0 + sseg * kSegCols;
-#pragma unroll 4
+    const int c0 = n0 + pass * Cfg::kPassCols + sseg * kSegCols;
+    const bool all_ok = c0 + kSegCols <= V && (mask_id < c0 || mask_id >= c0 + kSegCols);
+    uint64_t cand = 0;
+#pragma unroll
     for (int c4 = 0; c4 < kSegCols; c4 += 4) {
       const float4 v4 = *reinterpret_cast<const float4*>(base + c4 * 4);
-      const float vv[4] = {v4.x, v4.y, v4.z, v4.w};
+      const float vv[4] = {v4.x * rs_row, v4.y * rs_row, v4.z * rs_row, v4.w * rs_row};
       bool ok[4];
       float cmax = -INFINITY;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int col = c0 + c4 + e;
-        ok[e] = col < V && col != mask_id;
+        ok[e] = all_ok || (col < V && col != mask_id);
         if (ok[e]) cmax = fmaxf(cmax, vv[e]);
       }
       if (cmax > m) {  // rescale the running sums to the new max
@@ -146,21 +223,42 @@ __global__ __launch_bounds__(kThreads, 2) void lmhead_kernel(const T* __restrict
         const float ex = fast_exp(x);
         s += ex;
         t += ex * x;
-        if (better(vv[e], c0 + c4 + e, tv[kK - 1], ti[kK - 1])) topk_insert(tv, ti, vv[e], c0 + c4 + e);
+        if (own_row && better(vv[e], c0 + c4 + e, bv, bi)) cand |= uint64_t(1) << (c4 + e);
+      }
+    }
+    // insert the candidates; the wave loops as often as its busiest lane has candidates
+    while (__any(cand != 0)) {
+      if (cand) {
+        const int pos = __builtin_ctzll(cand);
+        cand &= cand - 1;
+        const float v = *reinterpret_cast<const float*>(base + pos * 4) * rs_row;
+        if (better(v, c0 + pos, tv[kK - 1], ti[kK - 1])) topk_insert(tv, ti, v, c0 + pos);
       }
     }
     __syncthreads();
-  }
-  const int row = m0 + srow;
-  if (row < R) {
-    const size_t p = size_t(row) * part.P + size_t(slice) * kSegs + sseg;
-    part.m[p] = m;
-    part.s[p] = s;
-    part.t[p] = t;
+    }
+    if constexpr (!kListInMemory) refresh_bound();
+    if (kListInMemory && own_row) {
+      part.m[slot] = m;
+      part.s[slot] = s;
+      part.t[slot] = t;
 #pragma unroll
-    for (int k = 0; k < kK; ++k) {
-      part.tv[p * kK + k] = tv[k];
-      part.ti[p * kK + k] = ti[k];
+      for (int k = 0; k < kK; ++k) {
+        part.tv[slot * kK + k] = tv[k];
+        part.ti[slot * kK + k] = ti[k];
+      }
+    }
+  }
+  if (own_row && !kListInMemory) {
+    part.m[slot] = m;
+    part.s[slot] = s;
+    part.t[slot] = t;
+    {
+#pragma unroll
+      for (int k = 0; k < kK; ++k) {
+        part.tv[slot * kK + k] = tv[k];
+        part.ti[slot * kK + k] = ti[k];
+      }
     }
   }
 }
@@ -242,9 +340,11 @@ __global__ __launch_bounds__(256) void probe_kernel(const T* __restrict__ Hs, co
 }
 
 int slices_for(int R, int V) {
-  const int rt = cdiv(R, kRows), vt = cdiv(V, kCols);
+  const int rt = cdiv(R, tile_rows(R)), vt = cdiv(V, kCols);
   return std::max(1, std::min(vt, cdiv(kTargetWg, rt)));
 }
+
+int partials_per_row(int R, int V) { return slices_for(R, V) * (kThreads / tile_rows(R)); }
 
 Partials carve(void* ws, int R, int P) {
   Partials pt;
@@ -262,7 +362,7 @@ Partials carve(void* ws, int R, int P) {
 }  // namespace
 
 size_t lmhead_workspace(int R, int V) {
-  const size_t P = size_t(slices_for(R, V)) * kSegs;
+  const size_t P = size_t(partials_per_row(R, V));
   return size_t(R) * P * (3 + 2 * kK) * 4 + 256;
 }
 
@@ -271,22 +371,27 @@ hipError_t lmhead_partials(int dtype, const void* h, const void* w, int R, int d
                            hipStream_t s) {
   if (d <= 0 || d % (dtype ? 64 : 32)) return hipErrorInvalidValue;   // the mainloop runs stages in pairs
   const int ns = slices_for(R, V);
-  const int rt = cdiv(R, kRows), vt = cdiv(V, kCols);
-  Partials part = carve(ws, R, ns * kSegs);
+  const int bm = tile_rows(R);
+  const int rt = cdiv(R, bm), vt = cdiv(V, kCols);
+  Partials part = carve(ws, R, partials_per_row(R, V));
   const int grid = rt * ns;
+  auto go = [&](auto kern, auto* hp, auto* wp) {
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(kThreads), 0, s, hp, wp, R, d, V, row_scale, rs_idx, rs_n, rs_lim,
+                       scale, mask_id, rt, ns, vt, part);
+  };
+  const bf16_t* hb = static_cast<const bf16_t*>(h);
+  const bf16_t* wb = static_cast<const bf16_t*>(w);
+  const float* hf = static_cast<const float*>(h);
+  const float* wf = static_cast<const float*>(w);
   if (dtype)
-    hipLaunchKernelGGL(lmhead_kernel<bf16_t>, dim3(grid), dim3(kThreads), 0, s, static_cast<const bf16_t*>(h),
-                       static_cast<const bf16_t*>(w), R, d, V, row_scale, rs_idx, rs_n, rs_lim, scale, mask_id, rt,
-                       ns, vt, part);
+    bm == 256 ? go(lmhead_kernel<bf16_t, 256>, hb, wb) : go(lmhead_kernel<bf16_t, 128>, hb, wb);
   else
-    hipLaunchKernelGGL(lmhead_kernel<float>, dim3(grid), dim3(kThreads), 0, s, static_cast<const float*>(h),
-                       static_cast<const float*>(w), R, d, V, row_scale, rs_idx, rs_n, rs_lim, scale, mask_id, rt,
-                       ns, vt, part);
+    bm == 256 ? go(lmhead_kernel<float, 256>, hf, wf) : go(lmhead_kernel<float, 128>, hf, wf);
   return hipGetLastError();
 }
 
 hipError_t lmhead_merge(int R, int V, const StatsOut& out, void* ws, hipStream_t s) {
-  Partials part = carve(ws, R, slices_for(R, V) * kSegs);
+  Partials part = carve(ws, R, partials_per_row(R, V));
   hipLaunchKernelGGL(merge_kernel, dim3(cdiv(R, 4)), dim3(256), 0, s, part, R, out);
   return hipGetLastError();
 }
