@@ -63,20 +63,43 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(const T* __restrict__
   const int lc = lane & 15;
 
   if constexpr (EPI == EPI_RESID) {
-    const int col_base = tn * kBN + wn * TM::kWTN + lc;
+    // x += acc through LDS: each wave stages half of its 64 x 128 tile at a
+    // time (64 x 64 fp32, 16 KB, in its own region of the idle ring), rows of
+    // 16 chunks of 4 floats with chunk c of row r in slot c ^ (r % 16), so
+    // both the MFMA-layout writes and the row reads are conflict-free; then
+    // every lane reads 16 bytes of x per access, all loads first (clamped
+    // into the matrix) and the guarded stores after them.
+    static_assert(TM::kWTM == 64 && TM::kWTN == 128, "resid epilogue tiling");
+    uint8_t* st = smem + wave * (64 * 64 * 4);
+    auto slot_of = [](int r, int c4) { return r * 256 + (((c4 ^ (r & 15))) << 4); };
+    const int r0 = m0 + wm * 64;
 #pragma unroll
-    for (int m = 0; m < TM::kFM; ++m)
+    for (int h = 0; h < 2; ++h) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = row_base + m * 16 + i;
-        if (row >= M) continue;
-        float* xr = ep.x + size_t(row) * ep.ldx;
+      for (int m = 0; m < TM::kFM; ++m)
 #pragma unroll
-        for (int n = 0; n < TM::kFN; ++n) {
-          const int col = col_base + n * 16;
-          if (col < N) xr[col] += acc[m][n][i];
-        }
+        for (int nn = 0; nn < 4; ++nn)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int r = m * 16 + 4 * (lane >> 4) + i, c = nn * 16 + lc;
+            *reinterpret_cast<float*>(st + slot_of(r, c >> 2) + (c & 3) * 4) = acc[m][4 * h + nn][i];
+          }
+      const int c0 = tn * kBN + wn * TM::kWTN + 64 * h;
+      f32x4 xv[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int q = lane + 64 * j, r = q >> 4, c4 = q & 15;
+        const int row = min(r0 + r, M - 1), col = min(c0 + 4 * c4, N - 4);
+        xv[j] = *reinterpret_cast<const f32x4*>(ep.x + size_t(row) * ep.ldx + col);
       }
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int q = lane + 64 * j, r = q >> 4, c4 = q & 15;
+        const int row = r0 + r, col = c0 + 4 * c4;
+        const f32x4 a = *reinterpret_cast<const f32x4*>(st + slot_of(r, c4));
+        if (row < M && col < N) *reinterpret_cast<f32x4*>(ep.x + size_t(row) * ep.ldx + col) = xv[j] + a;
+      }
+    }
   } else if constexpr (EPI == EPI_SWIGLU) {
     T* out = reinterpret_cast<T*>(ep.out);
 #pragma unroll
@@ -220,6 +243,7 @@ hipError_t launch(const void* A, int lda, const void* B, int ldb, int M, int N, 
 
 hipError_t gemm_resid(int dtype, const void* A, int lda, const void* B, int ldb, int M, int N, int K, float* X,
                       int ldx, hipStream_t s) {
+  if (N % 4 || ldx % 4 || reinterpret_cast<uintptr_t>(X) % 16) return hipErrorInvalidValue;   // 16-byte x accesses
   EpiParams ep{};
   ep.x = X;
   ep.ldx = ldx;
