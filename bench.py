@@ -213,6 +213,20 @@ def other_configs(P, model, shape, n):
                     "commits_confidence": st.commits_conf, "commits_pivot": st.commits_pivot,
                     "abstains": st.abstains}
     log(f"{wl.name}: {wall:.2f} s, NFE {st.nfe}")
+
+    # the baselines of Section 3 on the same model, prompt and scales: Default
+    # (one most confident token per forward) and Confidence (threshold 0.9)
+    rps_row = out[wl.name]
+    for name, rule, k, tau in (("default", "confidence", 1, 0.0), ("confidence_tau0.9", "threshold", 1, wl.tau_conf)):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        toks_b, sb = P.baseline_decode(model, prompt, wl.gen_len, wl.block, rule, k=k, tau=tau, row_scale=scales)
+        torch.cuda.synchronize()
+        wall_b = time.perf_counter() - t0
+        rps_row[f"baseline_{name}"] = {"committed_tokens_per_s": round(wl.gen_len / wall_b, 2),
+                                       "wall_s": round(wall_b, 3), "nfe": sb.nfe}
+        rps_row[f"speedup_vs_{name}"] = {"nfe": round(sb.nfe / st.nfe, 2), "tps": round(wall_b / wall, 2)}
+        log(f"{wl.name} baseline {name}: {wall_b:.2f} s, NFE {sb.nfe}")
     return out
 
 

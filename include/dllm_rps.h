@@ -291,6 +291,24 @@ dllm_status rps_commit(int32_t* tokens, int32_t seq, int32_t* m_pos, int32_t n_m
                        const dllm_stats* anchor, float tau, int32_t* n_m_out,
                        int32_t* committed, int32_t* n_committed, dllm_stream stream);
 
+/* Baseline scheduler commit (Section 3, Eq. 2, first two cases; Eq. 1 for
+ * the assignment): the masked rows with the k highest confidences
+ * P^max = exp(lmax - lse) (SCHED_TOP_CONFIDENCE; k = 1 is the one-token-per-
+ * step Default decoder), or with the k lowest entropies H (SCHED_LOW_ENTROPY),
+ * ties to the lower row, i.e. the lower position (m_pos ascending).  The
+ * third case of Eq. 2, the confidence threshold, is rps_commit with
+ * dec = NULL and tau >= 0.
+ *   min(k, n_m) rows are committed: tokens[m_pos[j]] = stats->argmax[j];
+ *   m_pos and stats are compacted in place to the remaining rows, n_m_out
+ *   (device int32) receives the new |M|, committed [n_m] the committed
+ *   positions in row order and n_committed (device int32) their count.
+ * Errors: DLLM_EINVAL for NULL arguments, a rule outside the enum or k < 1;
+ * DLLM_ESHAPE for n_m outside 1 .. RPS_MAX_MASKED or seq < 1. */
+enum { SCHED_TOP_CONFIDENCE = 0, SCHED_LOW_ENTROPY = 1 };
+dllm_status sched_commit(int32_t* tokens, int32_t seq, int32_t* m_pos, int32_t n_m, const dllm_stats* stats,
+                         int32_t rule, int32_t k, int32_t* n_m_out, int32_t* committed, int32_t* n_committed,
+                         dllm_stream stream);
+
 #ifdef __cplusplus
 }
 #endif

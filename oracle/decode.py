@@ -97,6 +97,41 @@ def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps
     return res
 
 
+def baseline_decode(forward, prompt, gen_len: int, block: int, mask_id: int, rule: str, k: int = 1,
+                    tau: float = 0.9, max_iters: int = 100000) -> DecodeResult:
+    """The semi-autoregressive baselines of Section 3 (Eq. 1 and 2): blocks
+    left to right; inside a block every step is one forward over the current
+    sequence and a commit of S with greedy tokens, where S is the k most
+    confident masked positions (rule "confidence"; k = 1 is the Default
+    decoder), the k lowest-entropy ones (rule "entropy"), or every position
+    with P^max >= tau and else the most confident one (rule "threshold", the
+    Confidence baseline of Fast-dLLM).  Trace: ("commit", positions, margin)."""
+    prompt = np.asarray(prompt, dtype=np.int64)
+    P = len(prompt)
+    tokens = np.concatenate([prompt, np.full(gen_len, mask_id, dtype=np.int64)])
+    res = DecodeResult(tokens=tokens)
+    iters = 0
+    for b in range(gen_len // block):
+        m_pos = np.arange(P + b * block, P + (b + 1) * block)
+        m_pos = m_pos[tokens[m_pos] == mask_id]
+        while len(m_pos) > 0:
+            iters += 1
+            assert iters <= max_iters
+            stats = forward(tokens[None, :], m_pos, None)[0][0]
+            res.nfe += 1
+            res.normal += 1
+            state = rps.State(tokens, m_pos, stats)
+            if rule == "threshold":
+                committed, margin = rps.apply_confidence_commit(state, tau, mask_id)
+            else:
+                committed, margin = rps.apply_topk_commit(state, rule, k, mask_id)
+            res.commits_conf += len(committed)
+            res.trace.append(("commit", sorted(int(c) for c in committed), margin))
+            tokens, m_pos = state.tokens, state.m_pos
+    res.tokens = tokens
+    return res
+
+
 def model_forward(weights, shape, topk: int = 16, scales=None, scale: float = 1.0,
                   mirror: bool = False):
     """Forward callback for ``rps_decode`` backed by the oracle transformer.

@@ -96,6 +96,25 @@ def top_k_rows(values: np.ndarray, k: int) -> np.ndarray:
     return np.lexsort((np.arange(len(values)), -values))[:k]
 
 
+def topk_commit(st: Stats, rule: str, k: int):
+    """Rows committed by the top-k rules of Eq. 2: the k rows of highest
+    confidence (first case; ranked by log P^max = lmax - lse, the same order
+    as P^max) or of lowest entropy (second case; ranked by -H), the lower row
+    (= lower position) first on ties.  Returns (rows ascending, tokens =
+    argmax (Eq. 1), margin = gap between the k-th and (k+1)-th ranked keys)."""
+    if rule == "confidence":
+        key = np.asarray(st.lmax, dtype=np.float64) - np.asarray(st.lse, dtype=np.float64)
+    elif rule == "entropy":
+        key = -np.asarray(st.H, dtype=np.float64)
+    else:
+        raise ValueError(rule)
+    order = np.lexsort((np.arange(len(key)), -key))
+    k = min(k, len(key))
+    margin = float(key[order[k - 1]] - key[order[k]]) if k < len(key) else math.inf
+    rows = np.sort(order[:k])
+    return rows, st.argmax[rows], margin
+
+
 # ------------------------------------------------------------ pivot selection
 
 def truncated(st: Stats, k_max: int):
@@ -255,6 +274,19 @@ class State:
 def apply_confidence_commit(state: State, tau: float, mask_id: int):
     """Commit S (Eq. 2, third case) with greedy tokens (Eq. 1); returns committed positions."""
     rows, toks, margin = confidence_commit(state.stats, tau)
+    assert np.all(toks != mask_id)
+    state.tokens[state.m_pos[rows]] = toks
+    keep = np.setdiff1d(np.arange(len(state.m_pos)), rows)
+    committed = state.m_pos[rows].copy()
+    state.m_pos = state.m_pos[keep]
+    state.stats = state.stats.rows(keep)
+    return committed, margin
+
+
+def apply_topk_commit(state: State, rule: str, k: int, mask_id: int):
+    """Commit the top-k rule's rows (Eq. 2, first or second case) with greedy
+    tokens (Eq. 1); returns (committed positions ascending, margin)."""
+    rows, toks, margin = topk_commit(state.stats, rule, k)
     assert np.all(toks != mask_id)
     state.tokens[state.m_pos[rows]] = toks
     keep = np.setdiff1d(np.arange(len(state.m_pos)), rows)

@@ -9,10 +9,10 @@ from . import binding  # noqa: F401
 from .binding import (  # noqa: F401
     Stats, dllm_model_create, dllm_model_destroy, dllm_workspace_bytes, dllm_forward,
     vocab_entropy_topk, vocab_entropy_topk_workspace_bytes, rps_select_pivots, rps_build_branches,
-    rps_lookahead_score, rps_commit, params, new_plan, new_decision, read_plan, read_decision, lib,
+    rps_lookahead_score, rps_commit, sched_commit, params, new_plan, new_decision, read_plan, read_decision, lib,
     dllm_profile_begin, dllm_profile_end,
 )
 from .model import Model  # noqa: F401
-from .step import RpsStep, rps_decode  # noqa: F401
+from .step import RpsStep, rps_decode, baseline_decode  # noqa: F401
 
 lib()  # fail loudly here if the HIP library is missing

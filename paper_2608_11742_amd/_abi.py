@@ -89,7 +89,10 @@ SIGNATURES = {
     "rps_lookahead_score": (i32, [C.POINTER(StatsC), C.POINTER(StatsC), i32, i32, vp, vp, f32, vp, vp, vp, vp]),
     "rps_commit": (i32, [vp, i32, vp, i32, C.POINTER(StatsC), vp, C.POINTER(StatsC), i32, C.POINTER(StatsC), f32,
                          vp, vp, vp, vp]),
+    "sched_commit": (i32, [vp, i32, vp, i32, C.POINTER(StatsC), i32, i32, vp, vp, vp, vp]),
 }
+
+SCHED_TOP_CONFIDENCE, SCHED_LOW_ENTROPY = 0, 1
 
 
 def load(path: str = LIB_PATH):

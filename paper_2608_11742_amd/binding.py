@@ -198,3 +198,10 @@ def rps_commit(tokens, m_pos, n_m: int, base: Stats, tau: float, n_m_out, commit
                             None if branches is None else C.byref(branches.c()), branch_offset,
                             None if anchor is None else C.byref(anchor.c()), tau, _p(n_m_out), _p(committed),
                             _p(n_committed), _stream(stream)))
+
+
+def sched_commit(tokens, m_pos, n_m: int, stats: Stats, rule: int, k: int, n_m_out, committed, n_committed,
+                 stream=None):
+    """Baseline scheduler commit (Eq. 2, top-k by confidence or by lowest entropy)."""
+    _check(lib().sched_commit(_p(tokens), tokens.shape[-1], _p(m_pos), n_m, C.byref(stats.c()), rule, k,
+                              _p(n_m_out), _p(committed), _p(n_committed), _stream(stream)))

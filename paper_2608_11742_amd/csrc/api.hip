@@ -464,4 +464,20 @@ dllm_status rps_commit(int32_t* tokens, int32_t seq, int32_t* m_pos, int32_t n_m
                    "rps_commit");
 }
 
+dllm_status sched_commit(int32_t* tokens, int32_t seq, int32_t* m_pos, int32_t n_m, const dllm_stats* stats,
+                         int32_t rule, int32_t k, int32_t* n_m_out, int32_t* committed, int32_t* n_committed,
+                         dllm_stream stream) {
+  dllm_status st = check_stats(stats, "stats");
+  if (st != DLLM_OK) return st;
+  if (!tokens || !m_pos || !n_m_out || !committed || !n_committed)
+    return fail(DLLM_EINVAL, "sched_commit: NULL argument");
+  if (rule != SCHED_TOP_CONFIDENCE && rule != SCHED_LOW_ENTROPY) return fail(DLLM_EINVAL, "rule %d", rule);
+  if (k < 1) return fail(DLLM_EINVAL, "k %d", k);
+  if (n_m < 1 || n_m > RPS_MAX_MASKED) return fail(DLLM_ESHAPE, "n_m %d", n_m);
+  if (seq < 1) return fail(DLLM_ESHAPE, "seq %d", seq);
+  return hip_check(sched_commit_step(tokens, seq, m_pos, n_m, to_out(*stats), rule, k, n_m_out, committed,
+                                     n_committed, static_cast<hipStream_t>(stream)),
+                   "sched_commit");
+}
+
 }  // extern "C"

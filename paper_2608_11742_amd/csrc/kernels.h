@@ -82,5 +82,7 @@ hipError_t rps_score(const StatsOut& anchor, const StatsOut& branches, int branc
 hipError_t rps_commit_step(int32_t* tokens, int seq, int32_t* m_pos, int n_m, const StatsOut& base, const rps_decision* dec,
                            const StatsOut* branches, int branch_offset, const StatsOut* anchor, float tau,
                            int32_t* n_m_out, int32_t* committed, int32_t* n_committed, hipStream_t s);
+hipError_t sched_commit_step(int32_t* tokens, int seq, int32_t* m_pos, int n_m, const StatsOut& st, int rule, int k,
+                            int32_t* n_m_out, int32_t* committed, int32_t* n_committed, hipStream_t s);
 
 }  // namespace dllm

@@ -220,74 +220,16 @@ __global__ __launch_bounds__(kT) void score_kernel(StatsIn anc, StatsIn br, int 
   *dec = r;
 }
 
-__global__ __launch_bounds__(kT) void commit_kernel(int32_t* __restrict__ tokens, int seq, int32_t* __restrict__ m_pos,
-                                                    int n_m,
-                                                    StatsOut base, const rps_decision* __restrict__ dec,
-                                                    StatsIn brs, int branch_offset, StatsIn anc, int has_anchor,
-                                                    float tau, int32_t* __restrict__ n_m_out,
-                                                    int32_t* __restrict__ committed,
-                                                    int32_t* __restrict__ n_committed) {
-  __shared__ uint8_t sel[kMaxM];
-  __shared__ int pre[kMaxM];
-  __shared__ int wsum[kT / kWave];
-  __shared__ float red_v[4];
-  __shared__ int red_i[4];
-  __shared__ int s_drop, s_nc;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// Commit the rows flagged in sel (tokens[m_pos[j]] = argmax[j], Eq. 1) after
+// the s_nc positions already in committed[], then compact m_pos and the
+// statistics (from src into base, possibly in place) to the rows neither
+// selected nor equal to `drop`.  Called by all kT threads of the workgroup.
+__device__ void commit_compact(int32_t* __restrict__ tokens, int seq, int32_t* __restrict__ m_pos, int n_m,
+                               StatsOut base, StatsIn src, const uint8_t* sel, int* pre, int s_drop, int s_nc,
+                               int32_t* __restrict__ n_m_out, int32_t* __restrict__ committed,
+                               int32_t* __restrict__ n_committed) {
+  const int tid = threadIdx.x;
   const int K = base.k;
-
-  // source of the carried statistics
-  StatsIn src{base.H, base.lse, base.lmax, base.argmax, base.topk_id, base.topk_logit, base.k};
-  int drop = -1;
-  if (dec) {
-    if (dec->commit) {
-      const size_t off = size_t(branch_offset + dec->branch) * n_m;
-      src = StatsIn{brs.H + off, brs.lse + off, brs.lmax + off, brs.argmax + off,
-                    brs.topk_id + off * brs.k, brs.topk_logit + off * brs.k, brs.k};
-      drop = dec->pivot_row;
-    } else if (has_anchor) {
-      src = anc;
-    }
-  }
-  if (tid == 0) {
-    s_nc = 0;
-    s_drop = drop;
-    if (drop >= 0) {
-      tokens[min(max(dec->pivot_pos, 0), seq - 1)] = dec->token;
-      committed[0] = dec->pivot_pos;
-      s_nc = 1;
-    }
-  }
-  // confidence-aware commit on the carried statistics
-  int n_sel = 0;
-  for (int j = tid; j < n_m; j += kT) {
-    bool s = false;
-    if (tau >= 0.f && j != drop) s = expf(src.lmax[j] - src.lse[j]) >= tau;
-    sel[j] = s;
-  }
-  __syncthreads();
-  if (tau >= 0.f) {
-    int c = 0;
-    for (int j = tid; j < n_m; j += kT) c += sel[j];
-    for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
-    if (lane == 0) wsum[wave] = c;
-    __syncthreads();
-    n_sel = wsum[0] + wsum[1] + wsum[2] + wsum[3];
-    __syncthreads();
-    if (n_sel == 0 && n_m - (drop >= 0 ? 1 : 0) > 0) {  // fallback: the single most confident row
-      float bv = -INFINITY;
-      int bi = 0x7fffffff;
-      for (int j = tid; j < n_m; j += kT)
-        if (j != drop) {
-          const float pm = expf(src.lmax[j] - src.lse[j]);
-          if (better(pm, j, bv, bi)) { bv = pm; bi = j; }
-        }
-      block_argmax(bv, bi, red_v, red_i);
-      if (tid == 0) sel[bi] = 1;
-      n_sel = 1;
-      __syncthreads();
-    }
-  }
   // exclusive prefix sums of selected rows (commit order) and of kept rows (new index)
   if (tid == 0) {
     int cs = 0, ks = 0;
@@ -344,6 +286,101 @@ __global__ __launch_bounds__(kT) void commit_kernel(int32_t* __restrict__ tokens
   }
 }
 
+__global__ __launch_bounds__(kT) void commit_kernel(int32_t* __restrict__ tokens, int seq, int32_t* __restrict__ m_pos,
+                                                    int n_m,
+                                                    StatsOut base, const rps_decision* __restrict__ dec,
+                                                    StatsIn brs, int branch_offset, StatsIn anc, int has_anchor,
+                                                    float tau, int32_t* __restrict__ n_m_out,
+                                                    int32_t* __restrict__ committed,
+                                                    int32_t* __restrict__ n_committed) {
+  __shared__ uint8_t sel[kMaxM];
+  __shared__ int pre[kMaxM];
+  __shared__ int wsum[kT / kWave];
+  __shared__ float red_v[4];
+  __shared__ int red_i[4];
+  __shared__ int s_drop, s_nc;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+  // source of the carried statistics
+  StatsIn src{base.H, base.lse, base.lmax, base.argmax, base.topk_id, base.topk_logit, base.k};
+  int drop = -1;
+  if (dec) {
+    if (dec->commit) {
+      const size_t off = size_t(branch_offset + dec->branch) * n_m;
+      src = StatsIn{brs.H + off, brs.lse + off, brs.lmax + off, brs.argmax + off,
+                    brs.topk_id + off * brs.k, brs.topk_logit + off * brs.k, brs.k};
+      drop = dec->pivot_row;
+    } else if (has_anchor) {
+      src = anc;
+    }
+  }
+  if (tid == 0) {
+    s_nc = 0;
+    s_drop = drop;
+    if (drop >= 0) {
+      tokens[min(max(dec->pivot_pos, 0), seq - 1)] = dec->token;
+      committed[0] = dec->pivot_pos;
+      s_nc = 1;
+    }
+  }
+  // confidence-aware commit on the carried statistics
+  int n_sel = 0;
+  for (int j = tid; j < n_m; j += kT) {
+    bool s = false;
+    if (tau >= 0.f && j != drop) s = expf(src.lmax[j] - src.lse[j]) >= tau;
+    sel[j] = s;
+  }
+  __syncthreads();
+  if (tau >= 0.f) {
+    int c = 0;
+    for (int j = tid; j < n_m; j += kT) c += sel[j];
+    for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+    if (lane == 0) wsum[wave] = c;
+    __syncthreads();
+    n_sel = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+    __syncthreads();
+    if (n_sel == 0 && n_m - (drop >= 0 ? 1 : 0) > 0) {  // fallback: the single most confident row
+      float bv = -INFINITY;
+      int bi = 0x7fffffff;
+      for (int j = tid; j < n_m; j += kT)
+        if (j != drop) {
+          const float pm = expf(src.lmax[j] - src.lse[j]);
+          if (better(pm, j, bv, bi)) { bv = pm; bi = j; }
+        }
+      block_argmax(bv, bi, red_v, red_i);
+      if (tid == 0) sel[bi] = 1;
+      n_sel = 1;
+      __syncthreads();
+    }
+  }
+  commit_compact(tokens, seq, m_pos, n_m, base, src, sel, pre, s_drop, s_nc, n_m_out, committed, n_committed);
+}
+
+// Baseline schedulers of Eq. 2 (first two cases): commit the k rows of
+// highest confidence (key log P^max = lmax - lse) or of lowest entropy
+// (key -H); ties go to the lower row, i.e. the lower position.  A row is
+// selected iff fewer than k rows beat it, counted against every row in LDS.
+__global__ __launch_bounds__(kT) void sched_kernel(int32_t* __restrict__ tokens, int seq, int32_t* __restrict__ m_pos,
+                                                   int n_m, StatsOut base, int rule, int k,
+                                                   int32_t* __restrict__ n_m_out, int32_t* __restrict__ committed,
+                                                   int32_t* __restrict__ n_committed) {
+  __shared__ float key[kMaxM];
+  __shared__ uint8_t sel[kMaxM];
+  __shared__ int pre[kMaxM];
+  const int tid = threadIdx.x;
+  for (int j = tid; j < n_m; j += kT) key[j] = rule == SCHED_LOW_ENTROPY ? -base.H[j] : base.lmax[j] - base.lse[j];
+  __syncthreads();
+  for (int j = tid; j < n_m; j += kT) {
+    const float v = key[j];
+    int rank = 0;
+    for (int o = 0; o < n_m; ++o) rank += better(key[o], o, v, j);
+    sel[j] = rank < k;
+  }
+  __syncthreads();
+  const StatsIn src{base.H, base.lse, base.lmax, base.argmax, base.topk_id, base.topk_logit, base.k};
+  commit_compact(tokens, seq, m_pos, n_m, base, src, sel, pre, -1, 0, n_m_out, committed, n_committed);
+}
+
 StatsIn to_in(const StatsOut& s) { return StatsIn{s.H, s.lse, s.lmax, s.argmax, s.topk_id, s.topk_logit, s.k}; }
 
 }  // namespace
@@ -376,6 +413,13 @@ hipError_t rps_commit_step(int32_t* tokens, int seq, int32_t* m_pos, int n_m, co
   const StatsIn an = anchor ? to_in(*anchor) : StatsIn{};
   hipLaunchKernelGGL(commit_kernel, dim3(1), dim3(kT), 0, s, tokens, seq, m_pos, n_m, base, dec, br, branch_offset, an,
                      anchor ? 1 : 0, tau, n_m_out, committed, n_committed);
+  return hipGetLastError();
+}
+
+hipError_t sched_commit_step(int32_t* tokens, int seq, int32_t* m_pos, int n_m, const StatsOut& st, int rule, int k,
+                            int32_t* n_m_out, int32_t* committed, int32_t* n_committed, hipStream_t s) {
+  hipLaunchKernelGGL(sched_kernel, dim3(1), dim3(kT), 0, s, tokens, seq, m_pos, n_m, st, rule, k, n_m_out, committed,
+                     n_committed);
   return hipGetLastError();
 }
 

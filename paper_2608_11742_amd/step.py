@@ -10,6 +10,7 @@ from dataclasses import dataclass, field
 import torch
 
 from . import binding as B
+from . import _abi
 from ._abi import Probe, KvCache
 
 
@@ -160,3 +161,59 @@ def rps_decode(model, prompt, gen_len: int, block: int, prm, lam: float, tau: fl
                 st.abstains += 1
             n_m = n_new
     return tokens, st
+
+
+_SCHED_RULES = {"confidence": _abi.SCHED_TOP_CONFIDENCE, "entropy": _abi.SCHED_LOW_ENTROPY}
+
+
+def baseline_decode(model, prompt, gen_len: int, block: int, rule: str, k: int = 1, tau: float = 0.9,
+                    row_scale=None, scale: float = 1.0, topk: int = 16, timing: bool = False,
+                    record: bool = False):
+    """The semi-autoregressive baselines of Section 3 (Eq. 1 and 2) on the GPU.
+
+    Blocks left to right; every step is one forward over the sequence and one
+    commit of S with greedy tokens: the k most confident masked positions
+    (rule "confidence"; k = 1 is the Default decoder), the k lowest-entropy
+    ones (rule "entropy", sched_commit), or every position with P^max >= tau
+    and else the most confident one (rule "threshold", rps_commit without a
+    lookahead decision: the Confidence baseline).  Returns (tokens, DecodeStats);
+    record keeps ("commit", positions) per step.
+    """
+    if rule not in ("confidence", "entropy", "threshold"):
+        raise ValueError(f"unknown rule {rule!r}")
+    dev = prompt.device
+    P = prompt.shape[0]
+    S = P + gen_len
+    mask_id = model.shape.mask_id
+    tokens = torch.cat([prompt.to(torch.int32), torch.full((gen_len,), mask_id, dtype=torch.int32, device=dev)])
+    st = DecodeStats()
+    base = B.Stats(block, topk, device=dev)
+    n_m_out = torch.zeros(1, dtype=torch.int32, device=dev)
+    committed = torch.zeros(block, dtype=torch.int32, device=dev)
+    n_committed = torch.zeros(1, dtype=torch.int32, device=dev)
+    model.workspace(1, S, block)
+    ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) if timing else None
+    for b in range(gen_len // block):
+        m_pos = torch.arange(P + b * block, P + (b + 1) * block, dtype=torch.int32, device=dev)
+        n_m = block
+        while n_m > 0:
+            if ev:
+                ev[0].record()
+            model.forward(tokens[None], m_pos, out=base, n_lm_pos=n_m, row_scale=row_scale, scale=scale)
+            st.nfe += 1
+            st.normal += 1
+            if ev:
+                ev[1].record()
+                ev[1].synchronize()
+                st.normal_ms += ev[0].elapsed_time(ev[1])
+            if rule == "threshold":
+                B.rps_commit(tokens, m_pos, n_m, base, tau, n_m_out, committed, n_committed)
+            else:
+                B.sched_commit(tokens, m_pos, n_m, base, _SCHED_RULES[rule], k, n_m_out, committed, n_committed)
+            n_new = int(n_m_out.item())
+            st.commits_conf += n_m - n_new
+            if record:
+                st.trace.append(("commit", sorted(committed[:n_m - n_new].tolist())))
+            n_m = n_new
+    return tokens, st
+

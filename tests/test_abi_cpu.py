@@ -139,6 +139,12 @@ def test_scheduler_validation(abi):
     st8 = _stats(_abi, k=8)
     assert lib.rps_commit(fake, 64, fake, 32, C.byref(st), fake, C.byref(st8), 0, None, 0.9, fake, fake, fake,
                           None) == 1
+    # baseline scheduler commit: rule outside the enum, k < 1, |M| out of range, NULL arguments
+    assert lib.sched_commit(fake, 64, fake, 32, C.byref(st), 2, 1, fake, fake, fake, None) == 1
+    assert lib.sched_commit(fake, 64, fake, 32, C.byref(st), _abi.SCHED_LOW_ENTROPY, 0, fake, fake, fake, None) == 1
+    assert lib.sched_commit(fake, 64, fake, 0, C.byref(st), _abi.SCHED_TOP_CONFIDENCE, 1, fake, fake, fake, None) == 2
+    assert lib.sched_commit(fake, 64, fake, 2000, C.byref(st), 0, 1, fake, fake, fake, None) == 2
+    assert lib.sched_commit(None, 64, fake, 32, C.byref(st), 0, 1, fake, fake, fake, None) == 1
 
 
 def test_model_create_without_device_reports_hip_error(abi):

@@ -6,7 +6,7 @@ import torch
 
 import synth
 from oracle import rps as orps
-from oracle.decode import rps_decode as oracle_decode, model_forward
+from oracle.decode import rps_decode as oracle_decode, baseline_decode as oracle_baseline, model_forward
 from tests.parity import MARGIN
 
 pytestmark = pytest.mark.gpu
@@ -54,3 +54,35 @@ def test_decode_trajectory_matches_oracle(tiny, tau_pivot, lam, seed):
     assert np.all(got[Pl:] != shape.mask_id)
     print(f"nfe {st.nfe} (lookahead {st.lookahead}), pivot commits {st.commits_pivot}, "
           f"abstains {st.abstains}, first excluded event {excluded}")
+
+
+@pytest.mark.parametrize("rule,k,tau,seed", [("confidence", 1, 0.0, 4), ("confidence", 3, 0.0, 5),
+                                             ("entropy", 2, 0.0, 6), ("threshold", 0, 0.5, 7)])
+def test_baseline_trajectory_matches_oracle(tiny, rule, k, tau, seed):
+    """The GPU baseline schedulers (Eq. 2: top-k by confidence or by lowest
+    entropy, confidence threshold) commit the same positions, step by step, as
+    the oracle; a divergence is accepted only on a step whose ranking the oracle
+    itself places within the near-tie margin."""
+    P, shape, w_np, model = tiny
+    Pl, G, B = 16, 64, 32
+    prompt = synth.tokens_np(seed, "prompt", Pl, shape.vocab - 1)
+    scales = synth.position_scales_np(seed + 10, np.arange(Pl + G), 2.6, 16.0)
+    toks, st = P.baseline_decode(model, torch.from_numpy(prompt).to(DEV), G, B, rule, k=max(k, 1), tau=tau,
+                                 row_scale=torch.from_numpy(scales).to(DEV), record=True)
+    got = toks.cpu().numpy()
+    ref = oracle_baseline(model_forward(w_np, shape, scales=scales), prompt, G, B, shape.mask_id, rule, max(k, 1),
+                          tau=tau)
+    excluded = None
+    for i, (g, o) in enumerate(zip(st.trace, ref.trace)):
+        if tuple(g) != tuple(o[:2]):
+            assert o[2] <= MARGIN, f"step {i}: gpu {g} vs oracle {o}"
+            excluded = i
+            break
+    if excluded is None:
+        assert len(st.trace) == len(ref.trace) and st.nfe == ref.nfe
+        assert np.array_equal(got, ref.tokens)
+    if rule != "threshold":
+        assert st.nfe == (G // B) * -(-B // k)
+    assert np.all(got[Pl:] != shape.mask_id)
+    print(f"{rule} k={k} tau={tau}: nfe {st.nfe}, first excluded step {excluded}")
+
