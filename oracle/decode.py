@@ -43,7 +43,12 @@ class DecodeResult:
 
 
 def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps.Params,
-               lam: float, tau: float, capacity: int = 16, max_iters: int = 100000) -> DecodeResult:
+               lam: float, tau: float, capacity: int = 16, max_iters: int = 100000,
+               lookahead=None) -> DecodeResult:
+    """lookahead: optional model for the lookahead forward,
+    ``lookahead(batch_tokens, m_pos, probe, block_start, block_len)`` with the
+    return of ``forward`` (e.g. a packed forward, which may use that every
+    branch differs from the anchor inside the current block only)."""
     import dataclasses
     prm = dataclasses.replace(prm, max_branch=min(prm.max_branch, capacity - 1))   # slot 0: anchor
     prompt = np.asarray(prompt, dtype=np.int64)
@@ -78,7 +83,10 @@ def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps
             pv = plan.pivots[0]
             batch = rps.branch_tokens(state.tokens, plan, with_anchor=True)
             probe = [(pv.row, t) for t in pv.tokens]
-            outs = forward(batch, state.m_pos, probe)
+            if lookahead is None:
+                outs = forward(batch, state.m_pos, probe)
+            else:
+                outs = lookahead(batch, state.m_pos, probe, P + b * block, block)
             res.nfe += 1
             res.lookahead += 1
             anchor, anchor_probe = outs[0]
@@ -148,6 +156,33 @@ def model_forward(weights, shape, topk: int = 16, scales=None, scale: float = 1.
         for b in range(logits.shape[0]):
             st = softmax_stats(logits[b], topk)
             pl = None if probe is None else [float(logits[b][row, tok] - st.lse[row]) for row, tok in probe]
+            out.append((st, pl))
+        return out
+    return fwd
+
+
+def model_packed_lookahead(weights, shape, topk: int = 16, scales=None, scale: float = 1.0,
+                           mirror: bool = False):
+    """Lookahead callback for ``rps_decode`` that evaluates the anchor and its
+    branches as one packed sequence [x || x_b^(c_1) || ...] with the
+    branch-isolating mask (Section 4.1, lookahead scoring; Algorithm 1)."""
+    from .model import packed_logits
+    from .stats import softmax_stats
+
+    def fwd(batch, m_pos, probe, block_start, block_len):
+        batch = np.asarray(batch)
+        S, b0, B = batch.shape[1], block_start, block_len
+        outside = np.ones(S, dtype=bool)
+        outside[b0:b0 + B] = False
+        assert np.all(batch[1:, outside] == batch[0, outside]), "branches differ from the anchor outside the block"
+        tokens = np.concatenate([batch[0]] + [row[b0:b0 + B] for row in batch[1:]])
+        rs = None if scales is None else np.asarray(scales)[np.asarray(m_pos)]
+        logits = packed_logits(tokens, weights, shape, S, b0, B, batch.shape[0] - 1, m_pos, mirror=mirror,
+                               row_scale=rs, scale=scale)
+        out = []
+        for c in range(logits.shape[0]):
+            st = softmax_stats(logits[c], topk)
+            pl = None if probe is None else [float(logits[c][row, tok] - st.lse[row]) for row, tok in probe]
             out.append((st, pl))
         return out
     return fwd

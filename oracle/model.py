@@ -51,13 +51,17 @@ def rope(u: np.ndarray, pos: np.ndarray, base: float) -> np.ndarray:
     return np.concatenate([u1 * c - u2 * s, u1 * s + u2 * c], axis=-1)
 
 
-def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
+def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, mask: np.ndarray | None = None) -> np.ndarray:
     """Non-causal softmax attention: softmax(q k^T / sqrt(hd)) v over all keys.
 
-    q: [H, Sq, hd], k, v: [H, Sk, hd] -> [H, Sq, hd].
+    q: [H, Sq, hd], k, v: [H, Sk, hd] -> [H, Sq, hd].  mask: optional boolean
+    [Sq, Sk]; a query attends only to the keys where it is True (every row
+    needs at least one).
     """
     hd = q.shape[-1]
     s = q @ np.swapaxes(k, -1, -2) / np.sqrt(hd)
+    if mask is not None:
+        s = np.where(mask[None], s, -np.inf)
     s = s - s.max(axis=-1, keepdims=True)
     p = np.exp(s)
     p = p / p.sum(axis=-1, keepdims=True)
@@ -72,13 +76,14 @@ def _w(weights, name) -> np.ndarray:
     return np.asarray(weights[name], dtype=np.float64)
 
 
-def layer(x, weights, l, shape, pos, mirror=False, prefix_kv=None, collect=None):
+def layer(x, weights, l, shape, pos, mirror=False, prefix_kv=None, collect=None, mask=None):
     """One transformer layer on one sequence.
 
-    x: [S, d] residual stream.  prefix_kv: optional (k, v) of a cached prefix,
-    each [H, P, hd] (post-RoPE); the S block positions then attend to the
-    prefix keys followed by their own keys.  collect: optional list that
-    receives this layer's (k, v), each [H, S, hd].
+    x: [S, d] residual stream; pos: [S] position ids.  prefix_kv: optional
+    (k, v) of a cached prefix, each [H, P, hd] (post-RoPE); the S block
+    positions then attend to the prefix keys followed by their own keys.
+    collect: optional list that receives this layer's (k, v), each [H, S, hd].
+    mask: optional boolean [S, S] attention mask (no prefix).
     """
     R = bf16_round if mirror else (lambda t: t)
     S, d = x.shape
@@ -98,7 +103,7 @@ def layer(x, weights, l, shape, pos, mirror=False, prefix_kv=None, collect=None)
         vv = np.concatenate([prefix_kv[1], v], axis=1)
     else:
         kk, vv = k, v
-    o = attention(q, kk, vv).transpose(1, 0, 2).reshape(S, d)
+    o = attention(q, kk, vv, mask).transpose(1, 0, 2).reshape(S, d)
     o = R(o)
     x = x + o @ _w(weights, f"layers.{l}.wo").T
     b = R(rmsnorm(x, shape.rms_eps))
@@ -148,6 +153,68 @@ def forward_logits(tokens_batch, weights, shape, lm_pos, pos_offset=0, mirror=Fa
     for tokens in np.asarray(tokens_batch):
         h = hidden(tokens, weights, shape, pos_offset=pos_offset, mirror=mirror, prefix_kv=prefix_kv)
         out.append(lm_logits(h[np.asarray(lm_pos)], weights, shape, row_scale=row_scale, scale=scale))
+    return np.stack(out)
+
+
+def packed_layout(shared_len: int, block_start: int, block_len: int, n_branch: int, pos_offset: int = 0):
+    """Position ids and attention mask of a packed lookahead sequence
+    x_ahead = [x || x_b^(c_1) || ... || x_b^(c_n)] (Section 4.1, lookahead
+    scoring; Algorithm 1).
+
+    Rows 0 .. S-1 are the shared sequence x (the anchor); branch c occupies
+    rows S + c*B .. S + (c+1)*B - 1 and stands in for the block b =
+    block_start .. block_start+B-1 of x, so its rows take the block's position
+    ids.  The mask isolates the branches: a shared row sees every shared row;
+    a branch row sees the shared rows outside block b and the rows of its own
+    branch.  Returns (pos [T], mask [T, T]) with T = S + n*B.
+    """
+    S, b0, B = shared_len, block_start, block_len
+    T = S + n_branch * B
+    grp = np.full(T, -1)                      # -1: shared row, c: branch c
+    pos = pos_offset + np.arange(T)
+    for c in range(n_branch):
+        rows = slice(S + c * B, S + (c + 1) * B)
+        grp[rows] = c
+        pos[rows] = pos_offset + b0 + np.arange(B)
+    in_block = np.zeros(T, dtype=bool)
+    in_block[b0:b0 + B] = True
+    mask = np.zeros((T, T), dtype=bool)
+    for r in range(T):
+        if grp[r] < 0:
+            mask[r] = grp < 0
+        else:
+            mask[r] = ((grp < 0) & ~in_block) | (grp == grp[r])
+    return pos, mask
+
+
+def packed_hidden(tokens, weights, shape, shared_len, block_start, block_len, n_branch, pos_offset=0,
+                  mirror=False):
+    """Final normed hidden states of every row of a packed lookahead sequence
+    (tokens [S + n*B]); layout and mask of ``packed_layout``."""
+    tokens = np.asarray(tokens, dtype=np.int64)
+    pos, mask = packed_layout(shared_len, block_start, block_len, n_branch, pos_offset)
+    assert tokens.shape[0] == pos.shape[0]
+    x = _w(weights, "emb")[tokens]
+    for l in range(shape.n_layers):
+        x = layer(x, weights, l, shape, pos, mirror=mirror, mask=mask)
+    h = rmsnorm(x, shape.rms_eps)
+    return bf16_round(h) if mirror else h
+
+
+def packed_logits(tokens, weights, shape, shared_len, block_start, block_len, n_branch, lm_pos, pos_offset=0,
+                  mirror=False, row_scale=None, scale=1.0):
+    """Logits of a packed lookahead forward at positions lm_pos of the shared
+    sequence, for the anchor and then for every branch: [1 + n, len(lm_pos), V].
+    A branch reads its own row where the position lies in the block, else the
+    shared row.  row_scale: optional per-position scale indexed like lm_pos."""
+    S, b0, B = shared_len, block_start, block_len
+    h = packed_hidden(tokens, weights, shape, S, b0, B, n_branch, pos_offset, mirror)
+    lm_pos = np.asarray(lm_pos, dtype=np.int64)
+    out = []
+    for c in range(-1, n_branch):
+        rows = np.array([S + c * B + (p - b0) if c >= 0 and b0 <= p < b0 + B else p for p in lm_pos],
+                        dtype=np.int64)
+        out.append(lm_logits(h[rows], weights, shape, row_scale=row_scale, scale=scale))
     return np.stack(out)
 
 

@@ -7,7 +7,7 @@ import pytest
 
 import synth
 from oracle import rps
-from oracle.decode import rps_decode, model_forward
+from oracle.decode import rps_decode, model_forward, model_packed_lookahead
 from oracle.stats import softmax_stats
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -93,3 +93,36 @@ def test_tiny_model_decode_invariants():
     assert res.nfe <= G
     assert res.nfe == res.normal + res.lookahead
     assert res.lookahead + res.abstains >= 0
+
+
+def test_packed_lookahead_one_layer_takes_the_unpacked_decisions():
+    # With one layer the packed forward equals the batch of full branch
+    # sequences (up to summation order), so Algorithm 1 takes the same path.
+    shape = synth.ModelShape(n_layers=1, d_model=64, n_heads=4, head_dim=16, d_ffn=96, vocab=101)
+    w = synth.model_weights_np(shape, seed=4, dtype="f32")
+    P, G, B = 8, 32, 16
+    prompt = synth.tokens_np(3, "prompt", P, shape.vocab - 1)
+    scales = synth.position_scales_np(4, np.arange(P + G), 2.6, 16.0)
+    prm = rps.Params(mode="paper", k_max=8, tau_pivot=0.5, r=0.05, n_cand=8)
+    fwd = model_forward(w, shape, scales=scales)
+    a = rps_decode(fwd, prompt, G, B, shape.mask_id, prm, lam=0.1, tau=0.9)
+    b = rps_decode(fwd, prompt, G, B, shape.mask_id, prm, lam=0.1, tau=0.9,
+                   lookahead=model_packed_lookahead(w, shape, scales=scales))
+    assert a.lookahead > 0
+    assert np.array_equal(a.tokens, b.tokens)
+    assert [t[:-1] for t in a.trace] == [t[:-1] for t in b.trace]          # decisions; margins last
+    for ta, tb in zip(a.trace, b.trace):
+        assert ta[-1] == tb[-1] or abs(ta[-1] - tb[-1]) < 1e-9   # margins agree to rounding
+
+
+def test_packed_lookahead_decode_invariants():
+    shape = synth.TINY
+    w = synth.model_weights_np(shape, seed=0, dtype="f32")
+    P, G, B = 16, 32, 16
+    prompt = synth.tokens_np(1, "prompt", P, shape.vocab - 1)
+    scales = synth.position_scales_np(2, np.arange(P + G), 2.6, 16.0)
+    prm = rps.Params(mode="paper", k_max=10, tau_pivot=0.9, r=0.1, n_cand=10)
+    res = rps_decode(model_forward(w, shape, scales=scales), prompt, G, B, shape.mask_id, prm, lam=0.1, tau=0.9,
+                     lookahead=model_packed_lookahead(w, shape, scales=scales))
+    _check_trace(res, P, G, B, shape.mask_id)
+    assert res.nfe == res.normal + res.lookahead and res.nfe <= G
