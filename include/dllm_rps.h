@@ -163,6 +163,43 @@ dllm_status dllm_forward(dllm_model* m, const int32_t* tokens, int32_t batch, in
                          const dllm_probe* probe, const dllm_stats* out,
                          void* ws, size_t ws_bytes, dllm_stream stream);
 
+/* Packed lookahead forward (Section 4.1, lookahead scoring and Algorithm 1's
+ * x_ahead = [x || x_b^(c_1) || ... ]): one sequence holding the shared
+ * sequence (the anchor: prompt and response, pivot still masked) followed by
+ * n_branch copies of the current block, each with its pivot filled by one
+ * candidate, evaluated in one forward with a branch-isolating attention mask.
+ *   tokens       [shared_len + n_branch * block_len] int32.
+ *   block_start  first position of the current block in the shared sequence;
+ *                branch rows reuse the block's position ids.
+ *   mask         shared rows attend to the shared rows only; the rows of a
+ *                branch attend to the shared rows outside the block they stand
+ *                in for (block_start .. block_start+block_len-1) and to their
+ *                own block, never to another branch.  With one layer a
+ *                branch's rows equal an independent forward of the shared
+ *                sequence with the block replaced; with more layers the shared
+ *                rows' keys and values are those of the anchor (the packing
+ *                approximation).
+ *   lm_pos       [n_lm_pos] positions of the shared sequence (clamped to
+ *                0 .. shared_len-1).  `out` receives (1 + n_branch) * n_lm_pos
+ *                rows, in the order of the unpacked lookahead batch: rows
+ *                0 .. n_lm_pos-1 are the shared sequence at lm_pos, rows
+ *                (1+c)*n_lm_pos + j are branch c at lm_pos[j] (the shared row
+ *                when lm_pos[j] lies outside the block).  probe rows index
+ *                these rows.
+ *   row_scale    nullable [shared_len] float indexed by in-sequence position
+ *                (a branch row uses the scale of the position it copies).
+ *   Other arguments as dllm_forward (batch 1, no KV cache).  The workspace is
+ *   dllm_workspace_bytes_packed(m, shared_len, block_len, n_branch, n_lm_pos).
+ * Errors: DLLM_ESHAPE unless 1 <= n_lm_pos <= shared_len, block_len is a
+ *   power of two, n_branch >= 0, 0 <= block_start, block_start + block_len <=
+ *   shared_len and pos_offset + shared_len <= max_pos. */
+size_t dllm_workspace_bytes_packed(const dllm_model* m, int32_t shared_len, int32_t block_len, int32_t n_branch,
+                                   int32_t n_lm_pos);
+dllm_status dllm_forward_packed(dllm_model* m, const int32_t* tokens, int32_t shared_len, int32_t block_start,
+                                int32_t block_len, int32_t n_branch, int32_t pos_offset, const int32_t* lm_pos,
+                                int32_t n_lm_pos, const float* row_scale, float scale, const dllm_probe* probe,
+                                const dllm_stats* out, void* ws, size_t ws_bytes, dllm_stream stream);
+
 /* LM head with fused vocabulary statistics (the per-position quantities of
  * Section 3, Notation, that Eq. 1-4 consume): for each of R rows of final
  * normed hidden states, logits = scale * row_scale[r] * (hidden[r] W_lm^T),
@@ -252,6 +289,15 @@ dllm_status rps_select_pivots(const dllm_stats* base, const int32_t* m_pos, int3
  * the plan's branches repeat `tokens`. */
 dllm_status rps_build_branches(const int32_t* tokens, int32_t seq, const rps_plan* plan,
                                int32_t anchor_first, int32_t capacity, int32_t* out, dllm_stream stream);
+
+/* Packed lookahead sequence x_ahead = [x || x_b^(c_1) || ... ] (Algorithm 1,
+ * Section 4.1) for dllm_forward_packed: out[seq + capacity * block_len] int32
+ * is `tokens`, then for slot b the block block_start .. block_start +
+ * block_len - 1 of `tokens` with br_pos[b] := br_token[b] (the unchanged block
+ * for slots beyond the plan's branches).  Errors: DLLM_ESHAPE unless 0 <=
+ * capacity <= RPS_MAX_BRANCH and the block lies inside 0 .. seq-1. */
+dllm_status rps_build_packed(const int32_t* tokens, int32_t seq, const rps_plan* plan, int32_t block_start,
+                             int32_t block_len, int32_t capacity, int32_t* out, dllm_stream stream);
 
 /* Lookahead scoring (Eq. 4) and the commit/abstain decision.
  *   anchor    statistics of the anchor branch (pivot still masked), n_m rows.

@@ -78,14 +78,18 @@ SIGNATURES = {
     "dllm_model_create": (i32, [C.POINTER(ModelDesc), C.POINTER(Weights), C.POINTER(vp)]),
     "dllm_model_destroy": (None, [vp]),
     "dllm_workspace_bytes": (sz, [vp, i32, i32, i32]),
+    "dllm_workspace_bytes_packed": (sz, [vp, i32, i32, i32, i32]),
     "dllm_forward": (i32, [vp, vp, i32, i32, i32, C.POINTER(KvCache), C.POINTER(KvCache), vp, i32, vp, f32,
                            C.POINTER(Probe), C.POINTER(StatsC), vp, sz, vp]),
+    "dllm_forward_packed": (i32, [vp, vp, i32, i32, i32, i32, i32, vp, i32, vp, f32, C.POINTER(Probe),
+                                  C.POINTER(StatsC), vp, sz, vp]),
     "vocab_entropy_topk_workspace_bytes": (sz, [i32, i32]),
     "vocab_entropy_topk": (i32, [vp, vp, i32, i32, i32, i32, vp, f32, i32, C.POINTER(StatsC), vp, sz, vp]),
     "dllm_profile_begin": (i32, [vp, i32]),
     "dllm_profile_end": (i32, [vp, C.POINTER(f32), C.POINTER(i32)]),
     "rps_select_pivots": (i32, [C.POINTER(StatsC), vp, i32, C.POINTER(RpsParams), vp, vp]),
     "rps_build_branches": (i32, [vp, i32, vp, i32, i32, vp, vp]),
+    "rps_build_packed": (i32, [vp, i32, vp, i32, i32, i32, vp, vp]),
     "rps_lookahead_score": (i32, [C.POINTER(StatsC), C.POINTER(StatsC), i32, i32, vp, vp, f32, vp, vp, vp, vp]),
     "rps_commit": (i32, [vp, i32, vp, i32, C.POINTER(StatsC), vp, C.POINTER(StatsC), i32, C.POINTER(StatsC), f32,
                          vp, vp, vp, vp]),

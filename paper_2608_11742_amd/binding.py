@@ -150,6 +150,10 @@ def dllm_workspace_bytes(handle, batch: int, seq: int, n_lm_pos: int) -> int:
     return lib().dllm_workspace_bytes(handle, batch, seq, n_lm_pos)
 
 
+def dllm_workspace_bytes_packed(handle, shared_len: int, block_len: int, n_branch: int, n_lm_pos: int) -> int:
+    return lib().dllm_workspace_bytes_packed(handle, shared_len, block_len, n_branch, n_lm_pos)
+
+
 def dllm_forward(handle, tokens, lm_pos, out: Stats, ws, pos_offset: int = 0, row_scale=None, scale: float = 1.0,
                  kv_prefix: KvCache | None = None, kv_out: KvCache | None = None, probe: Probe | None = None,
                  n_lm_pos: int | None = None, stream=None):
@@ -160,6 +164,18 @@ def dllm_forward(handle, tokens, lm_pos, out: Stats, ws, pos_offset: int = 0, ro
                               None if kv_out is None else C.byref(kv_out), _p(lm_pos), n_lm, _p(row_scale),
                               scale, None if probe is None else C.byref(probe), C.byref(out.c()), _p(ws),
                               ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def dllm_forward_packed(handle, tokens, shared_len: int, block_start: int, block_len: int, n_branch: int, lm_pos,
+                        out: Stats, ws, pos_offset: int = 0, row_scale=None, scale: float = 1.0,
+                        probe: Probe | None = None, n_lm_pos: int | None = None, stream=None):
+    """Packed lookahead forward: tokens [shared_len + n_branch * block_len] (one
+    sequence); out receives (1 + n_branch) * n_lm_pos rows (shared, then each branch)."""
+    n_lm = lm_pos.shape[0] if n_lm_pos is None else n_lm_pos
+    _check(lib().dllm_forward_packed(handle, _p(tokens), shared_len, block_start, block_len, n_branch, pos_offset,
+                                     _p(lm_pos), n_lm, _p(row_scale), scale,
+                                     None if probe is None else C.byref(probe), C.byref(out.c()), _p(ws),
+                                     ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def vocab_entropy_topk_workspace_bytes(R: int, vocab: int) -> int:
@@ -184,6 +200,12 @@ def rps_select_pivots(base: Stats, m_pos, n_m: int, prm: RpsParams, plan, stream
 def rps_build_branches(tokens, plan, anchor_first: bool, capacity: int, out, stream=None):
     _check(lib().rps_build_branches(_p(tokens), tokens.shape[-1], _p(plan), int(anchor_first), capacity, _p(out),
                                     _stream(stream)))
+
+
+def rps_build_packed(tokens, plan, block_start: int, block_len: int, capacity: int, out, stream=None):
+    """out[seq + capacity * block_len]: tokens, then one block copy per branch slot."""
+    _check(lib().rps_build_packed(_p(tokens), tokens.shape[-1], _p(plan), block_start, block_len, capacity, _p(out),
+                                  _stream(stream)))
 
 
 def rps_lookahead_score(anchor: Stats, branches: Stats, branch_offset: int, n_m: int, plan, lam: float, dec,

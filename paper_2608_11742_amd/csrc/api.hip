@@ -90,11 +90,17 @@ dllm_status check_stats(const dllm_stats* s, const char* name) {
 
 // Workspace layout of one forward (256-byte aligned regions).
 struct FwdLayout {
-  size_t x, a, q, k, vt, f, hl, lm, total;
+  size_t x, a, q, k, vt, f, hl, lm, lmsrc, total;
   int vt_ld;
 };
 
-FwdLayout plan_forward(const dllm_model_desc& d, int batch, int seq, int n_lm_pos) {
+// packed lookahead layout of one forward (see dllm_forward_packed)
+struct Packing {
+  int S, b0, B, n_branch;
+};
+
+// R: LM-head rows of the call (batch * n_lm_pos, or (1 + n_branch) * n_lm_pos packed)
+FwdLayout plan_forward(const dllm_model_desc& d, int batch, int seq, int R) {
   FwdLayout L;
   const size_t T = elem_bytes(d.dtype);
   const size_t M = size_t(batch) * seq;
@@ -111,9 +117,9 @@ FwdLayout plan_forward(const dllm_model_desc& d, int batch, int seq, int n_lm_po
   L.k = take(M * d.d_model * T);
   L.vt = take(size_t(batch) * d.n_heads * d.head_dim * L.vt_ld * T);
   L.f = take(M * d.d_ffn * T);
-  const int R = batch * n_lm_pos;
   L.hl = take(size_t(R) * d.d_model * T);
   L.lm = take(lmhead_workspace(R, d.vocab));
+  L.lmsrc = take(size_t(R) * 8);
   L.total = off;
   return L;
 }
@@ -230,22 +236,38 @@ dllm_status dllm_profile_end(dllm_model* m, float* ms, int32_t* launches) {
 
 size_t dllm_workspace_bytes(const dllm_model* m, int32_t batch, int32_t seq, int32_t n_lm_pos) {
   if (!m || batch < 1 || seq < 1 || n_lm_pos < 1) return 0;
-  return plan_forward(m->desc, batch, seq, n_lm_pos).total;
+  return plan_forward(m->desc, batch, seq, batch * n_lm_pos).total;
 }
 
-dllm_status dllm_forward(dllm_model* m, const int32_t* tokens, int32_t batch, int32_t seq, int32_t pos_offset,
+size_t dllm_workspace_bytes_packed(const dllm_model* m, int32_t shared_len, int32_t block_len, int32_t n_branch,
+                                   int32_t n_lm_pos) {
+  if (!m || shared_len < 1 || block_len < 1 || n_branch < 0 || n_lm_pos < 1) return 0;
+  return plan_forward(m->desc, 1, shared_len + n_branch * block_len, (1 + n_branch) * n_lm_pos).total;
+}
+
+namespace {
+
+dllm_status forward_impl(dllm_model* m, const int32_t* tokens, int32_t batch, int32_t seq, int32_t pos_offset,
                          const dllm_kv_cache* kv_prefix, const dllm_kv_cache* kv_out, const int32_t* lm_pos,
                          int32_t n_lm_pos, const float* row_scale, float scale, const dllm_probe* probe,
-                         const dllm_stats* out, void* ws, size_t ws_bytes, dllm_stream stream) {
+                         const dllm_stats* out, void* ws, size_t ws_bytes, dllm_stream stream, const Packing* pk) {
   if (!m) return fail(DLLM_EINVAL, "dllm_forward: NULL model");
   if (!tokens || !lm_pos || !ws) return fail(DLLM_EINVAL, "dllm_forward: NULL tokens, lm_pos or ws");
   dllm_status st = check_stats(out, "out");
   if (st != DLLM_OK) return st;
   const dllm_model_desc& d = m->desc;
-  if (batch < 1 || seq < 1 || n_lm_pos < 1 || n_lm_pos > seq)
+  if (batch < 1 || seq < 1 || n_lm_pos < 1 || n_lm_pos > (pk ? pk->S : seq))
     return fail(DLLM_ESHAPE, "batch %d seq %d n_lm_pos %d", batch, seq, n_lm_pos);
-  if (pos_offset < 0 || pos_offset + seq > d.max_pos)
-    return fail(DLLM_ESHAPE, "positions %d..%d exceed max_pos %d", pos_offset, pos_offset + seq - 1, d.max_pos);
+  const int n_pos = pk ? pk->S : seq;   // distinct positions of the call
+  if (pos_offset < 0 || pos_offset + n_pos > d.max_pos)
+    return fail(DLLM_ESHAPE, "positions %d..%d exceed max_pos %d", pos_offset, pos_offset + n_pos - 1, d.max_pos);
+  if (pk) {
+    if (batch != 1 || kv_prefix || kv_out) return fail(DLLM_EINVAL, "packed lookahead: batch 1, no KV cache");
+    if (pk->S < 1 || pk->B < 1 || (pk->B & (pk->B - 1)) || pk->n_branch < 0 || seq != pk->S + pk->n_branch * pk->B ||
+        pk->b0 < 0 || pk->b0 + pk->B > pk->S)
+      return fail(DLLM_ESHAPE, "packed lookahead: shared %d block %d..%d, seq %d", pk->S, pk->b0, pk->b0 + pk->B - 1,
+                  seq);
+  }
   if (!std::isfinite(scale)) return fail(DLLM_EINVAL, "scale is not finite");
   const size_t T = elem_bytes(d.dtype);
   const size_t M = size_t(batch) * seq;
@@ -264,7 +286,9 @@ dllm_status dllm_forward(dllm_model* m, const int32_t* tokens, int32_t batch, in
   }
   if (probe && probe->n > 0 && (!probe->row || !probe->token || !probe->logit))
     return fail(DLLM_EINVAL, "probe has a NULL array");
-  const FwdLayout L = plan_forward(d, batch, seq, n_lm_pos);
+  // LM-head rows: every sequence's n_lm_pos rows; packed: the anchor's, then each branch's
+  const int R = (pk ? 1 + pk->n_branch : batch) * n_lm_pos;
+  const FwdLayout L = plan_forward(d, batch, seq, R);
   if (ws_bytes < L.total) return fail(DLLM_ENOMEM, "workspace %zu < %zu bytes", ws_bytes, L.total);
 
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -278,6 +302,20 @@ dllm_status dllm_forward(dllm_model* m, const int32_t* tokens, int32_t batch, in
   void* hl = base + L.hl;
   const int dm = d.d_model, F = d.d_ffn, H = d.n_heads, hd = d.head_dim, dt = d.dtype;
   const int Mi = int(M);
+  // gathered row of each LM-head row (indexed modulo lm_n, per sequence) and
+  // its row-scale index (its in-sequence position)
+  const int32_t* lm_row = lm_pos;
+  const int32_t* rs_idx = lm_pos;
+  int lm_n = n_lm_pos;
+  if (pk) {
+    int32_t* rows = reinterpret_cast<int32_t*>(base + L.lmsrc);
+    ProfScope ps(m, s, DLLM_PROF_OTHER);
+    TRY_HIP(packed_lm_rows(pk->S, pk->b0, pk->B, pk->n_branch, lm_pos, n_lm_pos, rows, rows + R, s),
+            "packed LM-head rows");
+    lm_row = rows;
+    rs_idx = rows + R;
+    lm_n = R;
+  }
 
   {
     ProfScope ps(m, s, DLLM_PROF_EMBED);
@@ -289,6 +327,11 @@ dllm_status dllm_forward(dllm_model* m, const int32_t* tokens, int32_t batch, in
       TRY_HIP(rmsnorm(dt, x, dm, d.rms_eps, Mi, nullptr, 1, seq, a, s), "rmsnorm");
     }
     QkvOut qo{q, k, vt, seq, L.vt_ld, pos_offset, H, hd, dm, m->rope};
+    if (pk) {
+      qo.pack_S = pk->S;
+      qo.pack_b0 = pk->b0;
+      qo.pack_B = pk->B;
+    }
     {
       ProfScope ps(m, s, DLLM_PROF_GEMM_QKV);
       TRY_HIP(gemm_qkv(dt, a, dm, m->wqkv[l], Mi, dm, qo, s), "gemm_qkv");
@@ -317,6 +360,11 @@ dllm_status dllm_forward(dllm_model* m, const int32_t* tokens, int32_t batch, in
       aa.p_cap = kv_prefix->cap;
     }
     aa.o = a;
+    if (pk) {
+      aa.pack_S = pk->S;
+      aa.pack_b0 = pk->b0;
+      aa.pack_B = pk->B;
+    }
     {
       ProfScope ps(m, s, DLLM_PROF_ATTENTION);
       TRY_HIP(attention(dt, aa, s), "attention");
@@ -338,14 +386,13 @@ dllm_status dllm_forward(dllm_model* m, const int32_t* tokens, int32_t batch, in
       TRY_HIP(gemm_resid(dt, f, F, m->wdown[l], F, Mi, dm, F, x, dm, s), "gemm_down");
     }
   }
-  const int R = batch * n_lm_pos;
   {
     ProfScope ps(m, s, DLLM_PROF_RMSNORM);
-    TRY_HIP(rmsnorm(dt, x, dm, d.rms_eps, R, lm_pos, n_lm_pos, seq, hl, s), "final rmsnorm");
+    TRY_HIP(rmsnorm(dt, x, dm, d.rms_eps, R, lm_row, lm_n, seq, hl, s), "final rmsnorm");
   }
   {
     ProfScope ps(m, s, DLLM_PROF_LMHEAD);
-    TRY_HIP(lmhead_partials(dt, hl, m->lm_head, R, dm, d.vocab, row_scale, lm_pos, n_lm_pos, seq, scale,
+    TRY_HIP(lmhead_partials(dt, hl, m->lm_head, R, dm, d.vocab, row_scale, rs_idx, lm_n, n_pos, scale,
                             d.mask_id, base + L.lm, s),
             "lm head");
   }
@@ -355,11 +402,32 @@ dllm_status dllm_forward(dllm_model* m, const int32_t* tokens, int32_t batch, in
   }
   if (probe && probe->n > 0) {
     ProfScope ps(m, s, DLLM_PROF_OTHER);
-    TRY_HIP(probe_logits(dt, hl, m->lm_head, dm, d.vocab, R, probe->row, probe->token, probe->n, row_scale, lm_pos,
-                         n_lm_pos, seq, scale, probe->logit, s),
+    TRY_HIP(probe_logits(dt, hl, m->lm_head, dm, d.vocab, R, probe->row, probe->token, probe->n, row_scale, rs_idx,
+                         lm_n, n_pos, scale, probe->logit, s),
             "probe");
   }
   return DLLM_OK;
+}
+
+}  // namespace
+
+dllm_status dllm_forward(dllm_model* m, const int32_t* tokens, int32_t batch, int32_t seq, int32_t pos_offset,
+                         const dllm_kv_cache* kv_prefix, const dllm_kv_cache* kv_out, const int32_t* lm_pos,
+                         int32_t n_lm_pos, const float* row_scale, float scale, const dllm_probe* probe,
+                         const dllm_stats* out, void* ws, size_t ws_bytes, dllm_stream stream) {
+  return forward_impl(m, tokens, batch, seq, pos_offset, kv_prefix, kv_out, lm_pos, n_lm_pos, row_scale, scale, probe,
+                      out, ws, ws_bytes, stream, nullptr);
+}
+
+dllm_status dllm_forward_packed(dllm_model* m, const int32_t* tokens, int32_t shared_len, int32_t block_start,
+                                int32_t block_len, int32_t n_branch, int32_t pos_offset, const int32_t* lm_pos,
+                                int32_t n_lm_pos, const float* row_scale, float scale, const dllm_probe* probe,
+                                const dllm_stats* out, void* ws, size_t ws_bytes, dllm_stream stream) {
+  if (n_branch < 0 || block_len < 1 || shared_len < 1)
+    return fail(DLLM_ESHAPE, "packed lookahead: shared %d, %d branches of %d", shared_len, n_branch, block_len);
+  const Packing pk{shared_len, block_start, block_len, n_branch};
+  return forward_impl(m, tokens, 1, shared_len + n_branch * block_len, pos_offset, nullptr, nullptr, lm_pos,
+                      n_lm_pos, row_scale, scale, probe, out, ws, ws_bytes, stream, &pk);
 }
 
 size_t vocab_entropy_topk_workspace_bytes(int32_t R, int32_t vocab) {
@@ -416,6 +484,18 @@ dllm_status rps_build_branches(const int32_t* tokens, int32_t seq, const rps_pla
   return hip_check(rps_branches(tokens, seq, plan, anchor_first ? 1 : 0, capacity, out,
                                 static_cast<hipStream_t>(stream)),
                    "rps_build_branches");
+}
+
+dllm_status rps_build_packed(const int32_t* tokens, int32_t seq, const rps_plan* plan, int32_t block_start,
+                             int32_t block_len, int32_t capacity, int32_t* out, dllm_stream stream) {
+  if (!tokens || !plan || !out) return fail(DLLM_EINVAL, "rps_build_packed: NULL argument");
+  if (seq < 1 || capacity < 0 || capacity > RPS_MAX_BRANCH || block_len < 1 || block_start < 0 ||
+      block_start + block_len > seq)
+    return fail(DLLM_ESHAPE, "rps_build_packed: seq %d block %d..%d capacity %d", seq, block_start,
+                block_start + block_len - 1, capacity);
+  return hip_check(rps_branches_packed(tokens, seq, plan, block_start, block_len, capacity, out,
+                                       static_cast<hipStream_t>(stream)),
+                   "rps_build_packed");
 }
 
 dllm_status rps_lookahead_score(const dllm_stats* anchor, const dllm_stats* branches, int32_t branch_offset,

@@ -52,7 +52,7 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
-template <typename T, int HD>
+template <typename T, int HD, bool kPacked>
 __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_scale_log2) {
   using C = AttnCfg<T, HD>;
   __shared__ __attribute__((aligned(16))) uint8_t smem[2 * C::STAGE];
@@ -71,8 +71,31 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
   const uint8_t* Vp =
       a.kp ? reinterpret_cast<const uint8_t*>(static_cast<const T*>(a.vpt) + size_t(h) * HD * a.p_cap) : nullptr;
   const int n_pt = a.kp ? cdiv(a.p_len, kKT) : 0;
-  const int n_ot = cdiv(a.Sq, kKT);
-  const int n_tiles = n_pt + n_ot;
+  // Packed lookahead (pack_B > 0): the shared rows 0 .. S-1 attend to each
+  // other only; a branch block's rows attend to the shared rows outside the
+  // block they stand in for (b0 .. b0+pack_B-1) and to their own block.
+  // Phase 1 tiles cover keys 0 .. S-1, phase 2 tiles the branch blocks that
+  // hold this workgroup's branch queries, each block on tiles of its own.
+  constexpr bool packed = kPacked;   // a.pack_B > 0
+  const int S = packed ? a.pack_S : a.Sq;
+  const int n_ot = cdiv(S, kKT);
+  int jb0 = 0, tpb = 1, n_bt = 0;
+  if (packed) {
+    const int qlo = max(int(blockIdx.x) * kQT, S), qhi = min(int(blockIdx.x) * kQT + kQT, a.Sq);
+    if (qlo < qhi) {
+      jb0 = (qlo - S) / a.pack_B;
+      tpb = cdiv(a.pack_B, kKT);
+      n_bt = ((qhi - 1 - S) / a.pack_B - jb0 + 1) * tpb;
+    }
+  }
+  const int n_tiles = n_pt + n_ot + n_bt;
+  // branch of each of this lane's two query columns (-1: a shared row)
+  int qbr[2];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    const int q = q0 + qb * 16 + fr;
+    qbr[qb] = packed && q >= S ? (q - S) / a.pack_B : -1;
+  }
 
   // Q fragments (B operand of S^T = K Q^T): query q0 + 16 qb + fr, chunk 4 step + g
   u32x4 qf[2][C::QSTEPS];
@@ -91,10 +114,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
     const uint8_t* k;
     const uint8_t* v;
     int k0, nk, ld;
+    int branch;   // phase-2 tile: the branch block it covers; -1 otherwise
   };
   auto src = [&](int t) -> Src {
-    if (t < n_pt) return Src{Kp, Vp, t * kKT, a.p_len, a.p_cap};
-    return Src{Ko, Vo, (t - n_pt) * kKT, a.Sq, a.vt_ld};
+    if (t < n_pt) return Src{Kp, Vp, t * kKT, a.p_len, a.p_cap, -1};
+    if (t < n_pt + n_ot) return Src{Ko, Vo, (t - n_pt) * kKT, S, a.vt_ld, -1};
+    const int u = t - n_pt - n_ot, j = jb0 + u / tpb;
+    return Src{Ko, Vo, S + j * a.pack_B + (u % tpb) * kKT, S + (j + 1) * a.pack_B, a.vt_ld, j};
   };
   // Copy tile t into ring slot `slot`.  Lane l of a load instruction fills
   // row l / C, slot l % C of its block and fetches the chunk the swizzle
@@ -162,6 +188,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
     const uint8_t* sv = s + C::KB;
     const Src sr = src(t);
     const int k0 = sr.k0, nk = sr.nk;
+    // does the packing mask keys of this tile?  phase 2 always; phase 1 where
+    // the tile meets the stood-in block and the workgroup has branch queries
+    const bool pmask = packed && (sr.branch >= 0 || (n_bt > 0 && k0 < a.pack_b0 + a.pack_B && k0 + kKT > a.pack_b0));
 
     // the tile's 64 keys in two halves of 32: S^T, online softmax and P V per half
 #pragma unroll
@@ -182,7 +211,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
       // online softmax per query column (this lane's query q0 + 16 qb + fr)
       float p[2][2][4];
       float alpha[2];
-      const bool full = k0 + 32 * half + 32 <= nk;   // every key of this half is valid
+      const bool full = !pmask && k0 + 32 * half + 32 <= nk;   // every key of this half is valid
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
         float mt = -INFINITY;
@@ -191,13 +220,20 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int key = k0 + (2 * half + kk) * 16 + 4 * g + i;
-            const float v = (full || key < nk) ? sc[kk][qb][i] : -INFINITY;
+            bool ok = key < nk;
+            if (pmask)
+              ok = ok && (sr.branch >= 0 ? qbr[qb] == sr.branch
+                                         : (qbr[qb] < 0 || key < a.pack_b0 || key >= a.pack_b0 + a.pack_B));
+            const float v = (full || ok) ? sc[kk][qb][i] : -INFINITY;
             p[kk][qb][i] = v;
             mt = fmaxf(mt, v);
           }
         mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
         mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-        const float mnew = fmaxf(mrun[qb], mt * qk_scale_log2);
+        float mnew = fmaxf(mrun[qb], mt * qk_scale_log2);
+        // packed: a branch query can meet a tile whose keys it all masks
+        // before any key it sees; exponents then use 0 and give 0, not NaN
+        if constexpr (kPacked) mnew = mnew == -INFINITY ? 0.f : mnew;
         alpha[qb] = __builtin_amdgcn_exp2f(mrun[qb] - mnew);
         mrun[qb] = mnew;
         float ls = 0.f;
@@ -296,8 +332,14 @@ template <typename T, int HD>
 hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
   // the V^T copies read whole 16-byte chunks inside each row of pitch vt_ld / p_cap
   if (a.vt_ld < 8 || a.vt_ld % 8 || (a.kp && (a.p_cap < 8 || a.p_cap % 8))) return hipErrorInvalidValue;
+  if (a.pack_B > 0 && (a.B != 1 || a.kp || a.pack_S < 1 || a.pack_S > a.Sq || (a.Sq - a.pack_S) % a.pack_B ||
+                       a.pack_b0 < 0 || a.pack_b0 + a.pack_B > a.pack_S))
+    return hipErrorInvalidValue;
   const float scale = 1.4426950408889634f / sqrtf(float(HD));
-  hipLaunchKernelGGL((attn_kernel<T, HD>), dim3(cdiv(a.Sq, kQT), a.H, a.B), dim3(kThreads), 0, s, a, scale);
+  if (a.pack_B > 0)
+    hipLaunchKernelGGL((attn_kernel<T, HD, true>), dim3(cdiv(a.Sq, kQT), a.H, a.B), dim3(kThreads), 0, s, a, scale);
+  else
+    hipLaunchKernelGGL((attn_kernel<T, HD, false>), dim3(cdiv(a.Sq, kQT), a.H, a.B), dim3(kThreads), 0, s, a, scale);
   return hipGetLastError();
 }
 

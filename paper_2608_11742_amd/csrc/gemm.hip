@@ -127,11 +127,15 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(const T* __restrict__
     // rotary embedding in registers: (x1, x2) = columns (dim, dim + hd/2) of one head
     if (which < 2) {
 #pragma unroll
-      for (int m = 0; m < TM::kFM; ++m)
+      for (int m = 0; m < TM::kFM; ++m) {
+        // one 16-row block at a time: keeps the cos/sin loads of all blocks
+        // from being hoisted together into the registers
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int row = min(row_base + m * 16 + i, M - 1);
-          const int pos = o.pos_offset + row % o.seq;
+          const int r = row % o.seq;
+          const int pos = o.pos_offset + (o.pack_B && r >= o.pack_S ? o.pack_b0 + ((r - o.pack_S) & (o.pack_B - 1)) : r);
 #pragma unroll
           for (int n = 0; n < TM::kFN; ++n) {
             if constexpr (true) {
@@ -144,6 +148,8 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(const T* __restrict__
             }
           }
         }
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
     if constexpr (Elem<T>::bytes == 2) {
       // stage the wave's 64 x 128 tile as bf16 in LDS (V transposed), then write

@@ -16,6 +16,10 @@ struct QkvOut {
   void* vt;          // [B][H][hd][vt_ld]
   int seq, vt_ld, pos_offset, H, hd, d;
   const float2* rope;  // [max_pos][hd/2] (cos, sin)
+  // packed lookahead (see AttnArgs): row r >= pack_S has the position of row
+  // pack_b0 + (r - pack_S) % pack_B (pack_B a power of two); pack_B == 0: row
+  // r has pos_offset + r
+  int pack_S = 0, pack_b0 = 0, pack_B = 0;
 };
 
 // X[M][N] (fp32, row stride ldx) += A[M][K] B[N][K]^T
@@ -44,8 +48,18 @@ struct AttnArgs {
   const void* vpt;   // prefix values^T [H][hd][cap]
   int p_len, p_cap;
   void* o;           // [B*Sq][H*hd]
+  // packed lookahead (B == 1, no prefix): rows 0 .. pack_S-1 are the shared
+  // sequence, then branch blocks of pack_B rows, each standing in for rows
+  // pack_b0 .. pack_b0+pack_B-1; pack_B == 0: no packing
+  int pack_S = 0, pack_b0 = 0, pack_B = 0;
 };
 hipError_t attention(int dtype, const AttnArgs& a, hipStream_t s);
+
+// LM-head rows of a packed lookahead forward: (1 + n_branch) * n_lm rows, the
+// shared sequence's then each branch's; row[] is the packed row each reads,
+// src[] its in-sequence position (the row-scale index)
+hipError_t packed_lm_rows(int S, int b0, int B, int n_branch, const int32_t* lm_pos, int n_lm, int32_t* row,
+                          int32_t* src, hipStream_t s);
 
 // copy this call's K and V^T (batch 1) into a cache at positions off .. off+seq-1
 hipError_t kv_store(int dtype, const void* k, const void* vt, int H, int seq, int hd, int vt_ld, void* ck,
@@ -76,6 +90,10 @@ hipError_t rps_select(const StatsOut& base, const int32_t* m_pos, int n_m, const
                       hipStream_t s);
 hipError_t rps_branches(const int32_t* tokens, int seq, const rps_plan* plan, int anchor_first, int capacity,
                         int32_t* out, hipStream_t s);
+// packed lookahead tokens: out[seq + capacity * B] = tokens, then one copy of
+// the block b0 .. b0+B-1 per branch slot with that branch's pivot filled
+hipError_t rps_branches_packed(const int32_t* tokens, int seq, const rps_plan* plan, int b0, int B, int capacity,
+                               int32_t* out, hipStream_t s);
 hipError_t rps_score(const StatsOut& anchor, const StatsOut& branches, int branch_offset, int n_m,
                      const rps_plan* plan, const float* anchor_logit, float lambda, float* scores, float* deltas,
                      rps_decision* dec, hipStream_t s);

@@ -99,4 +99,29 @@ hipError_t kv_store(int dtype, const void* k, const void* vt, int H, int seq, in
   return hipGetLastError();
 }
 
+namespace {
+
+// LM-head row t = c * n_lm + j reads position lm_pos[j] of sequence c: the
+// shared sequence for c = 0, branch c-1's copy of the block for c >= 1 when
+// the position lies in the block (else the shared row)
+__global__ void packed_lm_rows_kernel(int S, int b0, int B, int R, const int32_t* __restrict__ lm_pos, int n_lm,
+                                      int32_t* __restrict__ row, int32_t* __restrict__ src) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= R) return;
+  const int c = t / n_lm;
+  const int p = min(max(lm_pos[t - c * n_lm], 0), S - 1);
+  row[t] = (c > 0 && p >= b0 && p < b0 + B) ? S + (c - 1) * B + (p - b0) : p;
+  src[t] = p;
+}
+
+}  // namespace
+
+hipError_t packed_lm_rows(int S, int b0, int B, int n_branch, const int32_t* lm_pos, int n_lm, int32_t* row,
+                          int32_t* src, hipStream_t s) {
+  const int R = (1 + n_branch) * n_lm;
+  hipLaunchKernelGGL(packed_lm_rows_kernel, dim3(cdiv(R, 256)), dim3(256), 0, s, S, b0, B, R, lm_pos, n_lm, row,
+                     src);
+  return hipGetLastError();
+}
+
 }  // namespace dllm

@@ -162,6 +162,24 @@ __global__ __launch_bounds__(kT) void branch_kernel(const int32_t* __restrict__ 
   out[size_t(slot) * seq + s] = v;
 }
 
+// packed lookahead sequence: slot 0 (blockIdx.y) copies the shared sequence,
+// slot 1 + b writes branch b's copy of the block at seq + b * B
+__global__ __launch_bounds__(kT) void packed_branch_kernel(const int32_t* __restrict__ tokens, int seq,
+                                                           const rps_plan* __restrict__ plan, int b0, int B,
+                                                           int32_t* __restrict__ out) {
+  const int slot = blockIdx.y;
+  const int s = blockIdx.x * kT + threadIdx.x;
+  if (slot == 0) {
+    if (s < seq) out[s] = tokens[s];
+    return;
+  }
+  if (s >= B) return;
+  const int b = slot - 1, p = b0 + s;
+  int v = tokens[p];
+  if (b < plan->n_branch && plan->br_pos[b] == p) v = plan->br_token[b];
+  out[seq + size_t(b) * B + s] = v;
+}
+
 __global__ __launch_bounds__(kT) void score_kernel(StatsIn anc, StatsIn br, int branch_offset, int n_m,
                                                    const rps_plan* __restrict__ plan,
                                                    const float* __restrict__ anchor_logit, float lambda,
@@ -395,6 +413,13 @@ hipError_t rps_branches(const int32_t* tokens, int seq, const rps_plan* plan, in
                         int32_t* out, hipStream_t s) {
   hipLaunchKernelGGL(branch_kernel, dim3(cdiv(seq, kT), capacity), dim3(kT), 0, s, tokens, seq, plan, anchor_first,
                      out);
+  return hipGetLastError();
+}
+
+hipError_t rps_branches_packed(const int32_t* tokens, int seq, const rps_plan* plan, int b0, int B, int capacity,
+                               int32_t* out, hipStream_t s) {
+  hipLaunchKernelGGL(packed_branch_kernel, dim3(cdiv(std::max(seq, B), kT), 1 + capacity), dim3(kT), 0, s, tokens,
+                     seq, plan, b0, B, out);
   return hipGetLastError();
 }
 

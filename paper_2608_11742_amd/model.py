@@ -47,11 +47,16 @@ class Model:
         except Exception:
             pass
 
-    def workspace(self, batch: int, seq: int, n_lm_pos: int):
-        need = B.dllm_workspace_bytes(self.handle, batch, seq, n_lm_pos)
+    def _reserve(self, need: int):
         if self._ws is None or self._ws.numel() < need:
             self._ws = torch.empty(need, dtype=torch.uint8, device=self.device)
         return self._ws
+
+    def workspace(self, batch: int, seq: int, n_lm_pos: int):
+        return self._reserve(B.dllm_workspace_bytes(self.handle, batch, seq, n_lm_pos))
+
+    def workspace_packed(self, shared_len: int, block_len: int, n_branch: int, n_lm_pos: int):
+        return self._reserve(B.dllm_workspace_bytes_packed(self.handle, shared_len, block_len, n_branch, n_lm_pos))
 
     def new_kv_cache(self, cap: int):
         """Device buffers for a prefix cache of `cap` positions (cap rounded up to 8)."""
@@ -72,4 +77,18 @@ class Model:
         ws = self.workspace(tokens.shape[0], tokens.shape[1], n)
         B.dllm_forward(self.handle, tokens, lm_pos, out, ws, pos_offset=pos_offset, row_scale=row_scale, scale=scale,
                        kv_prefix=kv_prefix, kv_out=kv_out, probe=probe, n_lm_pos=n, stream=stream)
+        return out
+
+    def forward_packed(self, tokens, shared_len: int, block_start: int, block_len: int, n_branch: int, lm_pos,
+                       out: B.Stats | None = None, n_lm_pos: int | None = None, row_scale=None, scale: float = 1.0,
+                       pos_offset: int = 0, probe=None, k: int = 16, stream=None) -> B.Stats:
+        """Packed lookahead forward over [shared || n_branch block copies] (one
+        sequence, branch-isolating mask); returns (1 + n_branch) * n_lm_pos rows."""
+        n = lm_pos.shape[0] if n_lm_pos is None else n_lm_pos
+        if out is None:
+            out = B.Stats((1 + n_branch) * n, k, device=self.device)
+        ws = self.workspace_packed(shared_len, block_len, n_branch, n)
+        B.dllm_forward_packed(self.handle, tokens, shared_len, block_start, block_len, n_branch, lm_pos, out, ws,
+                              pos_offset=pos_offset, row_scale=row_scale, scale=scale, probe=probe, n_lm_pos=n,
+                              stream=stream)
         return out

@@ -78,13 +78,17 @@ class DecodeStats:
 
 
 def rps_decode(model, prompt, gen_len: int, block: int, prm, lam: float, tau: float, capacity: int = 16,
-               row_scale=None, scale: float = 1.0, k: int = 16, timing: bool = False, record: bool = False):
+               row_scale=None, scale: float = 1.0, k: int = 16, timing: bool = False, record: bool = False,
+               packed: bool = False):
     """Algorithm 1 on the GPU.  prompt: [P] int32 device.  Returns (tokens, DecodeStats).
 
     row_scale: optional [P + gen_len] per-position logit scales (device float32).
     record: keep a trace of every decision, ("commit", positions),
     ("skip",) and ("lookahead", pivot, token or -1), at the cost of one more
     read-back per standard commit.
+    packed: run each lookahead as one packed sequence [x || block copies] with
+    the branch-isolating mask (dllm_forward_packed) instead of a batch of
+    1 + n full sequences; block must then be a power of two.
     """
     if prm.max_branch > capacity - 1:
         raise ValueError("prm.max_branch must leave slot 0 of the lookahead batch to the anchor")
@@ -99,22 +103,32 @@ def rps_decode(model, prompt, gen_len: int, block: int, prm, lam: float, tau: fl
     plan = B.new_plan(dev)
     dec = B.new_decision(dev)
     bt = torch.empty(capacity, S, dtype=torch.int32, device=dev)
+    pk = torch.empty(S + (capacity - 1) * block, dtype=torch.int32, device=dev) if packed else None
     anchor_logit = torch.empty(16, dtype=torch.float32, device=dev)
     n_m_out = torch.zeros(1, dtype=torch.int32, device=dev)
     committed = torch.zeros(block, dtype=torch.int32, device=dev)
     n_committed = torch.zeros(1, dtype=torch.int32, device=dev)
-    model.workspace(capacity, S, block)
+    if packed:
+        model.workspace(1, S, block)
+        model.workspace_packed(S, block, capacity - 1, block)
+    else:
+        model.workspace(capacity, S, block)
     ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) if timing else None
 
-    def fwd(tok, n, out, probe=None, kind="normal"):
+    def fwd(tok, n, out, probe=None, kind="normal", nb=0):
         if ev:
             ev[0].record()
-        model.forward(tok, m_pos, out=out, n_lm_pos=n, row_scale=row_scale, scale=scale, probe=probe)
+        if kind == "packed":
+            model.forward_packed(tok, S, b0, block, nb, m_pos, out=out, n_lm_pos=n,
+                                 row_scale=row_scale, scale=scale, probe=probe)
+        else:
+            model.forward(tok, m_pos, out=out, n_lm_pos=n, row_scale=row_scale, scale=scale, probe=probe)
         st.nfe += 1
         if kind == "normal":
             st.normal += 1
         else:
             st.lookahead += 1
+            kind = "lookahead"
         if ev:
             ev[1].record()
             ev[1].synchronize()
@@ -125,7 +139,8 @@ def rps_decode(model, prompt, gen_len: int, block: int, prm, lam: float, tau: fl
                 st.lookahead_ms += ms
 
     for b in range(gen_len // block):
-        m_pos = torch.arange(P + b * block, P + (b + 1) * block, dtype=torch.int32, device=dev)
+        b0 = P + b * block
+        m_pos = torch.arange(b0, b0 + block, dtype=torch.int32, device=dev)
         n_m = block
         fwd(tokens[None], n_m, base)                                     # block-opening forward
         while n_m > 0:
@@ -143,10 +158,14 @@ def rps_decode(model, prompt, gen_len: int, block: int, prm, lam: float, tau: fl
                 fwd(tokens[None], n_m, base)
                 st.trace.append(("skip",))
                 continue
-            B.rps_build_branches(tokens, plan, True, 1 + nb, bt)
             probe = Probe(B.plan_field_ptr(plan, "br_row"), B.plan_field_ptr(plan, "br_token"),
                           anchor_logit.data_ptr(), nb)
-            fwd(bt[:1 + nb], n_m, branch, probe=probe, kind="lookahead")
+            if packed:
+                B.rps_build_packed(tokens, plan, b0, block, nb, pk)
+                fwd(pk[:S + nb * block], n_m, branch, probe=probe, kind="packed", nb=nb)
+            else:
+                B.rps_build_branches(tokens, plan, True, 1 + nb, bt)
+                fwd(bt[:1 + nb], n_m, branch, probe=probe, kind="lookahead")
             anchor = branch.rows(0, n_m)
             B.rps_lookahead_score(anchor, branch, 1, n_m, plan, lam, dec, anchor_logit=anchor_logit)
             B.rps_commit(tokens, m_pos, n_m, base, -1.0, n_m_out, committed, n_committed, dec=dec,

@@ -145,6 +145,15 @@ def test_scheduler_validation(abi):
     assert lib.sched_commit(fake, 64, fake, 0, C.byref(st), _abi.SCHED_TOP_CONFIDENCE, 1, fake, fake, fake, None) == 2
     assert lib.sched_commit(fake, 64, fake, 2000, C.byref(st), 0, 1, fake, fake, fake, None) == 2
     assert lib.sched_commit(None, 64, fake, 32, C.byref(st), 0, 1, fake, fake, fake, None) == 1
+    # packed lookahead tokens: block outside the sequence, capacity beyond RPS_MAX_BRANCH, NULL arguments
+    assert lib.rps_build_packed(fake, 64, fake, 48, 32, 4, fake, None) == 2
+    assert lib.rps_build_packed(fake, 64, fake, -1, 8, 4, fake, None) == 2
+    assert lib.rps_build_packed(fake, 64, fake, 0, 8, _abi.RPS_MAX_BRANCH + 1, fake, None) == 2
+    assert lib.rps_build_packed(fake, 64, None, 0, 8, 4, fake, None) == 1
+    # packed forward without a model
+    assert lib.dllm_forward_packed(None, fake, 64, 0, 8, 2, 0, fake, 4, None, 1.0, None, C.byref(st), fake, 1 << 20,
+                                   None) == 1
+    assert lib.dllm_workspace_bytes_packed(None, 64, 8, 2, 4) == 0
 
 
 def test_model_create_without_device_reports_hip_error(abi):
