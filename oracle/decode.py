@@ -44,12 +44,17 @@ class DecodeResult:
 
 def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps.Params,
                lam: float, tau: float, capacity: int = 16, max_iters: int = 100000,
-               lookahead=None) -> DecodeResult:
+               lookahead=None, block_forward=None) -> DecodeResult:
     """lookahead: optional model for the lookahead forward,
     ``lookahead(batch_tokens, m_pos, probe, block_start, block_len)`` with the
     return of ``forward`` (e.g. a packed forward, which may use that every
-    branch differs from the anchor inside the current block only)."""
+    branch differs from the anchor inside the current block only).
+    block_forward: optional ``block_forward(tokens, block_start)``, called at
+    every block opening, that returns the model used for every later forward
+    of that block (e.g. a prefix-cached model built from the opening state)."""
     import dataclasses
+    if lookahead is not None and block_forward is not None:
+        raise ValueError("a packed lookahead over a prefix cache is not modelled")
     prm = dataclasses.replace(prm, max_branch=min(prm.max_branch, capacity - 1))   # slot 0: anchor
     prompt = np.asarray(prompt, dtype=np.int64)
     P = len(prompt)
@@ -62,6 +67,7 @@ def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps
         stats = forward(tokens[None, :], m_pos, None)[0][0]
         res.nfe += 1
         res.normal += 1
+        fwd_b = forward if block_forward is None else block_forward(tokens.copy(), P + b * block)
         state = rps.State(tokens, m_pos, stats)
         while len(state.m_pos) > 0:
             iters += 1
@@ -75,7 +81,7 @@ def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps
             plan.pivots = plan.pivots[:1]
             brs = plan.branches()
             if not brs:
-                state.stats = forward(state.tokens[None, :], state.m_pos, None)[0][0]
+                state.stats = fwd_b(state.tokens[None, :], state.m_pos, None)[0][0]
                 res.nfe += 1
                 res.normal += 1
                 res.trace.append(("skip", plan.empty_margin))
@@ -84,7 +90,7 @@ def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps
             batch = rps.branch_tokens(state.tokens, plan, with_anchor=True)
             probe = [(pv.row, t) for t in pv.tokens]
             if lookahead is None:
-                outs = forward(batch, state.m_pos, probe)
+                outs = fwd_b(batch, state.m_pos, probe)
             else:
                 outs = lookahead(batch, state.m_pos, probe, P + b * block, block)
             res.nfe += 1
@@ -106,14 +112,16 @@ def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps
 
 
 def baseline_decode(forward, prompt, gen_len: int, block: int, mask_id: int, rule: str, k: int = 1,
-                    tau: float = 0.9, max_iters: int = 100000) -> DecodeResult:
+                    tau: float = 0.9, max_iters: int = 100000, block_forward=None) -> DecodeResult:
     """The semi-autoregressive baselines of Section 3 (Eq. 1 and 2): blocks
     left to right; inside a block every step is one forward over the current
     sequence and a commit of S with greedy tokens, where S is the k most
     confident masked positions (rule "confidence"; k = 1 is the Default
     decoder), the k lowest-entropy ones (rule "entropy"), or every position
     with P^max >= tau and else the most confident one (rule "threshold", the
-    Confidence baseline of Fast-dLLM).  Trace: ("commit", positions, margin)."""
+    Confidence baseline of Fast-dLLM).  Trace: ("commit", positions, margin).
+    block_forward: as in ``rps_decode``; the block's first step is the full
+    forward, every later step uses the model it returns."""
     prompt = np.asarray(prompt, dtype=np.int64)
     P = len(prompt)
     tokens = np.concatenate([prompt, np.full(gen_len, mask_id, dtype=np.int64)])
@@ -122,10 +130,13 @@ def baseline_decode(forward, prompt, gen_len: int, block: int, mask_id: int, rul
     for b in range(gen_len // block):
         m_pos = np.arange(P + b * block, P + (b + 1) * block)
         m_pos = m_pos[tokens[m_pos] == mask_id]
+        fwd_b = None
         while len(m_pos) > 0:
             iters += 1
             assert iters <= max_iters
-            stats = forward(tokens[None, :], m_pos, None)[0][0]
+            stats = (forward if fwd_b is None else fwd_b)(tokens[None, :], m_pos, None)[0][0]
+            if fwd_b is None:
+                fwd_b = forward if block_forward is None else block_forward(tokens.copy(), P + b * block)
             res.nfe += 1
             res.normal += 1
             state = rps.State(tokens, m_pos, stats)
@@ -186,3 +197,41 @@ def model_packed_lookahead(weights, shape, topk: int = 16, scales=None, scale: f
             out.append((st, pl))
         return out
     return fwd
+
+
+
+def model_prefix_cached(weights, shape, topk: int = 16, scales=None, scale: float = 1.0,
+                        mirror: bool = False):
+    """Block-forward factory for ``rps_decode`` and ``baseline_decode``: the
+    prefix cache the paper combines RPS with (Fast-dLLM's; Section 5.3, KV caching).
+
+    Reading: at a block opening the full forward over the whole sequence also
+    yields the per-layer keys and values of every position before the block;
+    they are kept, and every later forward of the block runs on the positions
+    from the block start to the end of the sequence (the block and the masked
+    suffix), attending to those cached keys and values plus its own.  Cached
+    rows do not see commits made after the block opened (the approximation).
+    """
+    from .model import hidden, lm_logits
+    from .stats import softmax_stats
+
+    def open_block(tokens, block_start):
+        kv = []
+        hidden(np.asarray(tokens), weights, shape, mirror=mirror, collect=kv)
+        ctx = [(k[:, :block_start], v[:, :block_start]) for k, v in kv] if block_start > 0 else None
+
+        def fwd(batch, m_pos, probe):
+            m_pos = np.asarray(m_pos)
+            rel = m_pos - block_start
+            assert np.all(rel >= 0), "LM rows must lie at or after the block start"
+            rs = None if scales is None else np.asarray(scales)[m_pos]
+            out = []
+            for toks in np.asarray(batch):
+                h = hidden(toks[block_start:], weights, shape, pos_offset=block_start, mirror=mirror, prefix_kv=ctx)
+                logits = lm_logits(h[rel], weights, shape, row_scale=rs, scale=scale)
+                st = softmax_stats(logits, topk)
+                pl = None if probe is None else [float(logits[row, tok] - st.lse[row]) for row, tok in probe]
+                out.append((st, pl))
+            return out
+        return fwd
+    return open_block

@@ -7,7 +7,7 @@ import pytest
 
 import synth
 from oracle import rps
-from oracle.decode import rps_decode, model_forward, model_packed_lookahead
+from oracle.decode import rps_decode, model_forward, model_packed_lookahead, model_prefix_cached
 from oracle.stats import softmax_stats
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -124,5 +124,65 @@ def test_packed_lookahead_decode_invariants():
     prm = rps.Params(mode="paper", k_max=10, tau_pivot=0.9, r=0.1, n_cand=10)
     res = rps_decode(model_forward(w, shape, scales=scales), prompt, G, B, shape.mask_id, prm, lam=0.1, tau=0.9,
                      lookahead=model_packed_lookahead(w, shape, scales=scales))
+    _check_trace(res, P, G, B, shape.mask_id)
+    assert res.nfe == res.normal + res.lookahead and res.nfe <= G
+
+
+def test_prefix_cached_forward_on_the_opening_tokens_is_the_full_forward():
+    # The cache holds the full forward's own keys and values, so a cached
+    # forward over unchanged tokens reproduces the full forward at any depth.
+    shape = synth.ModelShape(n_layers=2, d_model=64, n_heads=4, head_dim=16, d_ffn=96, vocab=101)
+    w = synth.model_weights_np(shape, seed=5, dtype="f32")
+    toks = synth.tokens_np(6, "t", 40, shape.vocab - 1)
+    toks[24:] = shape.mask_id
+    m_pos = np.arange(24, 32)
+    full = model_forward(w, shape)(toks[None], m_pos, [(1, 7)])
+    cached = model_prefix_cached(w, shape)(toks, 24)(toks[None], m_pos, [(1, 7)])
+    assert np.allclose(full[0][0].H, cached[0][0].H, atol=1e-10)
+    assert np.allclose(full[0][0].lse, cached[0][0].lse, atol=1e-10)
+    assert np.array_equal(full[0][0].topk_id, cached[0][0].topk_id)
+    assert abs(full[0][1][0] - cached[0][1][0]) < 1e-10
+    # after a commit inside the block the cached rows are stale: outputs differ
+    t2 = toks.copy()
+    t2[24] = 5
+    a = model_forward(w, shape)(t2[None], m_pos[1:], None)[0][0]
+    b = model_prefix_cached(w, shape)(toks, 24)(t2[None], m_pos[1:], None)[0][0]
+    assert not np.allclose(a.H, b.H, atol=1e-8)
+
+
+@pytest.mark.parametrize("decoder", ["rps", "confidence", "threshold"])
+def test_prefix_cache_with_one_layer_changes_nothing(decoder):
+    # With one layer every cached key and value depends on its own token and
+    # position only, so the cache is exact and the decode takes the same path.
+    shape = synth.ModelShape(n_layers=1, d_model=64, n_heads=4, head_dim=16, d_ffn=96, vocab=101)
+    w = synth.model_weights_np(shape, seed=7, dtype="f32")
+    P, G, B = 8, 48, 16
+    prompt = synth.tokens_np(8, "prompt", P, shape.vocab - 1)
+    scales = synth.position_scales_np(9, np.arange(P + G), 2.6, 16.0)
+    fwd = model_forward(w, shape, scales=scales)
+    cache = model_prefix_cached(w, shape, scales=scales)
+    if decoder == "rps":
+        prm = rps.Params(mode="paper", k_max=8, tau_pivot=0.5, r=0.05, n_cand=8)
+        a = rps_decode(fwd, prompt, G, B, shape.mask_id, prm, lam=0.1, tau=0.9)
+        b = rps_decode(fwd, prompt, G, B, shape.mask_id, prm, lam=0.1, tau=0.9, block_forward=cache)
+        assert a.lookahead > 0
+    else:
+        from oracle.decode import baseline_decode
+        k, tau = (2, 0.0) if decoder == "confidence" else (1, 0.6)
+        a = baseline_decode(fwd, prompt, G, B, shape.mask_id, decoder, k, tau=tau)
+        b = baseline_decode(fwd, prompt, G, B, shape.mask_id, decoder, k, tau=tau, block_forward=cache)
+    assert np.array_equal(a.tokens, b.tokens) and a.nfe == b.nfe
+    assert [t[:-1] for t in a.trace] == [t[:-1] for t in b.trace]
+
+
+def test_prefix_cached_decode_invariants():
+    shape = synth.TINY
+    w = synth.model_weights_np(shape, seed=0, dtype="f32")
+    P, G, B = 16, 64, 32
+    prompt = synth.tokens_np(1, "prompt", P, shape.vocab - 1)
+    scales = synth.position_scales_np(2, np.arange(P + G), 2.6, 16.0)
+    prm = rps.Params(mode="paper", k_max=10, tau_pivot=0.9, r=0.1, n_cand=10)
+    res = rps_decode(model_forward(w, shape, scales=scales), prompt, G, B, shape.mask_id, prm, lam=0.1, tau=0.9,
+                     block_forward=model_prefix_cached(w, shape, scales=scales))
     _check_trace(res, P, G, B, shape.mask_id)
     assert res.nfe == res.normal + res.lookahead and res.nfe <= G
