@@ -214,18 +214,44 @@ def other_configs(P, model, shape, n):
                     "abstains": st.abstains}
     log(f"{wl.name}: {wall:.2f} s, NFE {st.nfe}")
 
-    # the baselines of Section 3 on the same model, prompt and scales: Default
-    # (one most confident token per forward) and Confidence (threshold 0.9)
+    # the same decode with the lookahead packed into one sequence (branch-isolating
+    # mask), and with the prefix cache refreshed at every block opening
     rps_row = out[wl.name]
-    for name, rule, k, tau in (("default", "confidence", 1, 0.0), ("confidence_tau0.9", "threshold", 1, wl.tau_conf)):
+
+    def variant(**kw):
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        toks_b, sb = P.baseline_decode(model, prompt, wl.gen_len, wl.block, rule, k=k, tau=tau, row_scale=scales)
+        _, sv = P.rps_decode(model, prompt, wl.gen_len, wl.block, prm, wl.lam, wl.tau_conf,
+                             capacity=wl.capacity, row_scale=scales, timing=True, **kw)
+        torch.cuda.synchronize()
+        wall_v = time.perf_counter() - t0
+        return sv, wall_v, {"committed_tokens_per_s": round(wl.gen_len / wall_v, 2), "wall_s": round(wall_v, 3),
+                            "nfe": sv.nfe, "normal_forwards": sv.normal, "lookahead_forwards": sv.lookahead,
+                            "normal_ms_avg": round(sv.normal_ms / max(1, sv.normal), 2),
+                            "lookahead_ms_avg": round(sv.lookahead_ms / max(1, sv.lookahead), 2),
+                            "commits_pivot": sv.commits_pivot, "abstains": sv.abstains}
+    sp, wall_p, rps_row["packed_lookahead"] = variant(packed=True)
+    log(f"{wl.name} packed: {wall_p:.2f} s, NFE {sp.nfe}")
+    sc, wall_c, rps_row["prefix_cache"] = variant(prefix_cache=True)
+    log(f"{wl.name} prefix cache: {wall_c:.2f} s, NFE {sc.nfe}")
+
+    # the baselines of Section 3 on the same model, prompt and scales: Default
+    # (one most confident token per forward) and Confidence (threshold 0.9),
+    # the latter also with the prefix cache
+    for name, rule, k, tau, cache in (("default", "confidence", 1, 0.0, False),
+                                      ("confidence_tau0.9", "threshold", 1, wl.tau_conf, False),
+                                      ("confidence_tau0.9_prefix_cache", "threshold", 1, wl.tau_conf, True)):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        toks_b, sb = P.baseline_decode(model, prompt, wl.gen_len, wl.block, rule, k=k, tau=tau, row_scale=scales,
+                                       prefix_cache=cache)
         torch.cuda.synchronize()
         wall_b = time.perf_counter() - t0
         rps_row[f"baseline_{name}"] = {"committed_tokens_per_s": round(wl.gen_len / wall_b, 2),
                                        "wall_s": round(wall_b, 3), "nfe": sb.nfe}
-        rps_row[f"speedup_vs_{name}"] = {"nfe": round(sb.nfe / st.nfe, 2), "tps": round(wall_b / wall, 2)}
+        rps_row[f"speedup_vs_{name}"] = {"nfe": round(sb.nfe / st.nfe, 2), "tps": round(wall_b / wall, 2),
+                                         "tps_packed": round(wall_b / wall_p, 2),
+                                         "tps_prefix_cache": round(wall_b / wall_c, 2)}
         log(f"{wl.name} baseline {name}: {wall_b:.2f} s, NFE {sb.nfe}")
     return out
 

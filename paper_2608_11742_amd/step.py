@@ -77,9 +77,62 @@ class DecodeStats:
     trace: list = field(default_factory=list)
 
 
+class _BlockView:
+    """Where the forwards of one block run.  Without a prefix cache: the whole
+    sequence, absolute positions.  With the prefix cache (Fast-dLLM's, which
+    the paper combines RPS with; Section 5.3): the full forward that opens the
+    block writes every layer's keys and values into the cache, and the later
+    forwards of the block run on the block and the masked suffix only, at
+    positions relative to the block start, attending to the cached prefix."""
+
+    def __init__(self, model, tokens, row_scale, scale, prefix_cache: bool):
+        self.model, self.tokens, self.row_scale, self.scale = model, tokens, row_scale, scale
+        self.S = tokens.shape[0]
+        self.kv = None
+        if prefix_cache:
+            k, vt, cap = model.new_kv_cache(self.S)
+            self._kv_buf = (k, vt)
+            self.kv = KvCache(k.data_ptr(), vt.data_ptr(), 0, cap)
+        self.b0 = 0
+
+    def open(self, b0: int, block: int, out, n: int, probe=None):
+        """Full forward over the sequence at the block opening; returns the
+        block's masked positions in the view's coordinates."""
+        dev = self.tokens.device
+        m_abs = torch.arange(b0, b0 + block, dtype=torch.int32, device=dev)
+        self.b0 = b0
+        if self.kv is None:
+            self.model.forward(self.tokens[None], m_abs, out=out, n_lm_pos=n, row_scale=self.row_scale,
+                               scale=self.scale, probe=probe)
+            return m_abs
+        self.kv.len = 0
+        self.model.forward(self.tokens[None], m_abs, out=out, n_lm_pos=n, row_scale=self.row_scale,
+                           scale=self.scale, probe=probe, kv_out=self.kv)
+        self.kv.len = b0
+        return torch.arange(0, block, dtype=torch.int32, device=dev)
+
+    @property
+    def seq(self):
+        """The token sequence the block's later forwards and commits work on."""
+        return self.tokens if self.kv is None else self.tokens[self.b0:]
+
+    @property
+    def offset(self) -> int:
+        return 0 if self.kv is None else self.b0
+
+    def forward(self, tok, m_pos, out, n: int, probe=None):
+        if self.kv is None:
+            self.model.forward(tok, m_pos, out=out, n_lm_pos=n, row_scale=self.row_scale, scale=self.scale,
+                               probe=probe)
+            return
+        rs = None if self.row_scale is None else self.row_scale[self.b0:]
+        self.model.forward(tok, m_pos, out=out, n_lm_pos=n, row_scale=rs, scale=self.scale, probe=probe,
+                           pos_offset=self.b0, kv_prefix=self.kv if self.b0 > 0 else None)
+
+
 def rps_decode(model, prompt, gen_len: int, block: int, prm, lam: float, tau: float, capacity: int = 16,
                row_scale=None, scale: float = 1.0, k: int = 16, timing: bool = False, record: bool = False,
-               packed: bool = False):
+               packed: bool = False, prefix_cache: bool = False):
     """Algorithm 1 on the GPU.  prompt: [P] int32 device.  Returns (tokens, DecodeStats).
 
     row_scale: optional [P + gen_len] per-position logit scales (device float32).
@@ -89,9 +142,14 @@ def rps_decode(model, prompt, gen_len: int, block: int, prm, lam: float, tau: fl
     packed: run each lookahead as one packed sequence [x || block copies] with
     the branch-isolating mask (dllm_forward_packed) instead of a batch of
     1 + n full sequences; block must then be a power of two.
+    prefix_cache: refresh a prefix KV cache at every block opening and run the
+    block's later forwards (normal and lookahead) on the block and the masked
+    suffix only (see _BlockView).
     """
     if prm.max_branch > capacity - 1:
         raise ValueError("prm.max_branch must leave slot 0 of the lookahead batch to the anchor")
+    if packed and prefix_cache:
+        raise ValueError("packed lookahead over a prefix cache is not supported")
     dev = prompt.device
     P = prompt.shape[0]
     S = P + gen_len
@@ -102,7 +160,7 @@ def rps_decode(model, prompt, gen_len: int, block: int, prm, lam: float, tau: fl
     branch = B.Stats(capacity * block, k, device=dev)
     plan = B.new_plan(dev)
     dec = B.new_decision(dev)
-    bt = torch.empty(capacity, S, dtype=torch.int32, device=dev)
+    bt_buf = torch.empty(capacity * S, dtype=torch.int32, device=dev)
     pk = torch.empty(S + (capacity - 1) * block, dtype=torch.int32, device=dev) if packed else None
     anchor_logit = torch.empty(16, dtype=torch.float32, device=dev)
     n_m_out = torch.zeros(1, dtype=torch.int32, device=dev)
@@ -113,22 +171,18 @@ def rps_decode(model, prompt, gen_len: int, block: int, prm, lam: float, tau: fl
         model.workspace_packed(S, block, capacity - 1, block)
     else:
         model.workspace(capacity, S, block)
+    view = _BlockView(model, tokens, row_scale, scale, prefix_cache)
     ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) if timing else None
 
-    def fwd(tok, n, out, probe=None, kind="normal", nb=0):
+    def timed(kind, fn):
         if ev:
             ev[0].record()
-        if kind == "packed":
-            model.forward_packed(tok, S, b0, block, nb, m_pos, out=out, n_lm_pos=n,
-                                 row_scale=row_scale, scale=scale, probe=probe)
-        else:
-            model.forward(tok, m_pos, out=out, n_lm_pos=n, row_scale=row_scale, scale=scale, probe=probe)
+        r = fn()
         st.nfe += 1
         if kind == "normal":
             st.normal += 1
         else:
             st.lookahead += 1
-            kind = "lookahead"
         if ev:
             ev[1].record()
             ev[1].synchronize()
@@ -137,43 +191,48 @@ def rps_decode(model, prompt, gen_len: int, block: int, prm, lam: float, tau: fl
                 st.normal_ms += ms
             else:
                 st.lookahead_ms += ms
+        return r
 
     for b in range(gen_len // block):
         b0 = P + b * block
-        m_pos = torch.arange(b0, b0 + block, dtype=torch.int32, device=dev)
         n_m = block
-        fwd(tokens[None], n_m, base)                                     # block-opening forward
+        m_pos = timed("normal", lambda: view.open(b0, block, base, n_m))   # block-opening forward
+        seq, off = view.seq, view.offset
+        L = seq.shape[0]
+        bt = bt_buf[:capacity * L].view(capacity, L)
         while n_m > 0:
-            B.rps_commit(tokens, m_pos, n_m, base, tau, n_m_out, committed, n_committed)   # standard commit
+            B.rps_commit(seq, m_pos, n_m, base, tau, n_m_out, committed, n_committed)   # standard commit
             n_new = int(n_m_out.item())
             st.commits_conf += n_m - n_new
             if record:
-                st.trace.append(("commit", sorted(committed[:n_m - n_new].tolist())))
+                st.trace.append(("commit", sorted(int(c) + off for c in committed[:n_m - n_new].tolist())))
             n_m = n_new
             if n_m == 0:
                 break
             B.rps_select_pivots(base, m_pos, n_m, prm, plan)
             nb = B.read_plan(plan).n_branch
             if nb == 0:                                                  # skip rules: normal forward
-                fwd(tokens[None], n_m, base)
+                timed("normal", lambda: view.forward(seq[None], m_pos, base, n_m))
                 st.trace.append(("skip",))
                 continue
             probe = Probe(B.plan_field_ptr(plan, "br_row"), B.plan_field_ptr(plan, "br_token"),
                           anchor_logit.data_ptr(), nb)
             if packed:
                 B.rps_build_packed(tokens, plan, b0, block, nb, pk)
-                fwd(pk[:S + nb * block], n_m, branch, probe=probe, kind="packed", nb=nb)
+                timed("lookahead", lambda: model.forward_packed(pk[:S + nb * block], S, b0, block, nb, m_pos,
+                                                                out=branch, n_lm_pos=n_m, row_scale=row_scale,
+                                                                scale=scale, probe=probe))
             else:
-                B.rps_build_branches(tokens, plan, True, 1 + nb, bt)
-                fwd(bt[:1 + nb], n_m, branch, probe=probe, kind="lookahead")
+                B.rps_build_branches(seq, plan, True, 1 + nb, bt)
+                timed("lookahead", lambda: view.forward(bt[:1 + nb], m_pos, branch, n_m, probe=probe))
             anchor = branch.rows(0, n_m)
             B.rps_lookahead_score(anchor, branch, 1, n_m, plan, lam, dec, anchor_logit=anchor_logit)
-            B.rps_commit(tokens, m_pos, n_m, base, -1.0, n_m_out, committed, n_committed, dec=dec,
+            B.rps_commit(seq, m_pos, n_m, base, -1.0, n_m_out, committed, n_committed, dec=dec,
                          branches=branch, branch_offset=1, anchor=anchor)
             n_new = int(n_m_out.item())
             if record:
                 d = B.read_decision(dec)
-                st.trace.append(("lookahead", d.pivot_pos, d.token if d.commit else -1))
+                st.trace.append(("lookahead", d.pivot_pos + off, d.token if d.commit else -1))
             if n_new < n_m:
                 st.commits_pivot += 1
             else:
@@ -187,7 +246,7 @@ _SCHED_RULES = {"confidence": _abi.SCHED_TOP_CONFIDENCE, "entropy": _abi.SCHED_L
 
 def baseline_decode(model, prompt, gen_len: int, block: int, rule: str, k: int = 1, tau: float = 0.9,
                     row_scale=None, scale: float = 1.0, topk: int = 16, timing: bool = False,
-                    record: bool = False):
+                    record: bool = False, prefix_cache: bool = False):
     """The semi-autoregressive baselines of Section 3 (Eq. 1 and 2) on the GPU.
 
     Blocks left to right; every step is one forward over the sequence and one
@@ -196,7 +255,8 @@ def baseline_decode(model, prompt, gen_len: int, block: int, rule: str, k: int =
     ones (rule "entropy", sched_commit), or every position with P^max >= tau
     and else the most confident one (rule "threshold", rps_commit without a
     lookahead decision: the Confidence baseline).  Returns (tokens, DecodeStats);
-    record keeps ("commit", positions) per step.
+    record keeps ("commit", positions) per step.  prefix_cache: as in
+    rps_decode; a block's first step is its full opening forward.
     """
     if rule not in ("confidence", "entropy", "threshold"):
         raise ValueError(f"unknown rule {rule!r}")
@@ -211,14 +271,20 @@ def baseline_decode(model, prompt, gen_len: int, block: int, rule: str, k: int =
     committed = torch.zeros(block, dtype=torch.int32, device=dev)
     n_committed = torch.zeros(1, dtype=torch.int32, device=dev)
     model.workspace(1, S, block)
+    view = _BlockView(model, tokens, row_scale, scale, prefix_cache)
     ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) if timing else None
     for b in range(gen_len // block):
-        m_pos = torch.arange(P + b * block, P + (b + 1) * block, dtype=torch.int32, device=dev)
+        b0 = P + b * block
         n_m = block
+        m_pos = None
         while n_m > 0:
             if ev:
                 ev[0].record()
-            model.forward(tokens[None], m_pos, out=base, n_lm_pos=n_m, row_scale=row_scale, scale=scale)
+            if m_pos is None:
+                m_pos = view.open(b0, block, base, n_m)
+                seq, off = view.seq, view.offset
+            else:
+                view.forward(seq[None], m_pos, base, n_m)
             st.nfe += 1
             st.normal += 1
             if ev:
@@ -226,13 +292,12 @@ def baseline_decode(model, prompt, gen_len: int, block: int, rule: str, k: int =
                 ev[1].synchronize()
                 st.normal_ms += ev[0].elapsed_time(ev[1])
             if rule == "threshold":
-                B.rps_commit(tokens, m_pos, n_m, base, tau, n_m_out, committed, n_committed)
+                B.rps_commit(seq, m_pos, n_m, base, tau, n_m_out, committed, n_committed)
             else:
-                B.sched_commit(tokens, m_pos, n_m, base, _SCHED_RULES[rule], k, n_m_out, committed, n_committed)
+                B.sched_commit(seq, m_pos, n_m, base, _SCHED_RULES[rule], k, n_m_out, committed, n_committed)
             n_new = int(n_m_out.item())
             st.commits_conf += n_m - n_new
             if record:
-                st.trace.append(("commit", sorted(committed[:n_m - n_new].tolist())))
+                st.trace.append(("commit", sorted(int(c) + off for c in committed[:n_m - n_new].tolist())))
             n_m = n_new
     return tokens, st
-

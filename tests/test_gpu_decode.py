@@ -86,3 +86,60 @@ def test_baseline_trajectory_matches_oracle(tiny, rule, k, tau, seed):
     assert np.all(got[Pl:] != shape.mask_id)
     print(f"{rule} k={k} tau={tau}: nfe {st.nfe}, first excluded step {excluded}")
 
+
+
+@pytest.mark.parametrize("tau_pivot,lam,seed", [(0.9, 0.1, 11), (0.6, 0.3, 12)])
+def test_prefix_cached_decode_trajectory_matches_oracle(tiny, tau_pivot, lam, seed):
+    """Algorithm 1 with the prefix cache refreshed at every block opening: the
+    GPU loop (cache written by the opening forward, later forwards over the
+    block and suffix) takes the oracle's decisions."""
+    from oracle.decode import model_prefix_cached
+    P, shape, w_np, model = tiny
+    Pl, G, B = 16, 96, 32
+    prompt = synth.tokens_np(seed, "prompt", Pl, shape.vocab - 1)
+    scales = synth.position_scales_np(seed + 10, np.arange(Pl + G), 2.6, 16.0)
+    prm = P.params(mode="paper", k_max=10, tau_pivot=tau_pivot, n_pivots=1, r=0.1, n_cand=10, max_branch=15)
+    toks, st = P.rps_decode(model, torch.from_numpy(prompt).to(DEV), G, B, prm, lam, 0.9, capacity=16,
+                            row_scale=torch.from_numpy(scales).to(DEV), record=True, prefix_cache=True)
+    got = toks.cpu().numpy()
+    ref = oracle_decode(model_forward(w_np, shape, scales=scales), prompt, G, B, shape.mask_id,
+                        orps.Params(mode="paper", k_max=10, tau_pivot=tau_pivot, r=0.1, n_cand=10), lam, 0.9,
+                        capacity=16, block_forward=model_prefix_cached(w_np, shape, scales=scales))
+    excluded = None
+    for i, (g, o) in enumerate(zip(st.trace, ref.trace)):
+        if tuple(g) != tuple(_event_key(o)):
+            assert o[-1] <= MARGIN, f"event {i}: gpu {g} vs oracle {o}"
+            excluded = i
+            break
+    if excluded is None:
+        assert len(st.trace) == len(ref.trace)
+        assert np.array_equal(got, ref.tokens)
+        assert st.nfe == ref.nfe and st.lookahead == ref.lookahead
+    assert np.all(got[Pl:] != shape.mask_id)
+    print(f"prefix cache: nfe {st.nfe} (lookahead {st.lookahead}), pivot commits {st.commits_pivot}, "
+          f"abstains {st.abstains}, first excluded event {excluded}")
+
+
+@pytest.mark.parametrize("rule,k,tau,seed", [("confidence", 2, 0.0, 13), ("threshold", 0, 0.5, 14)])
+def test_prefix_cached_baseline_matches_oracle(tiny, rule, k, tau, seed):
+    from oracle.decode import model_prefix_cached
+    P, shape, w_np, model = tiny
+    Pl, G, B = 16, 96, 32
+    prompt = synth.tokens_np(seed, "prompt", Pl, shape.vocab - 1)
+    scales = synth.position_scales_np(seed + 10, np.arange(Pl + G), 2.6, 16.0)
+    toks, st = P.baseline_decode(model, torch.from_numpy(prompt).to(DEV), G, B, rule, k=max(k, 1), tau=tau,
+                                 row_scale=torch.from_numpy(scales).to(DEV), record=True, prefix_cache=True)
+    got = toks.cpu().numpy()
+    ref = oracle_baseline(model_forward(w_np, shape, scales=scales), prompt, G, B, shape.mask_id, rule, max(k, 1),
+                          tau=tau, block_forward=model_prefix_cached(w_np, shape, scales=scales))
+    excluded = None
+    for i, (g, o) in enumerate(zip(st.trace, ref.trace)):
+        if tuple(g) != tuple(o[:2]):
+            assert o[2] <= MARGIN, f"step {i}: gpu {g} vs oracle {o}"
+            excluded = i
+            break
+    if excluded is None:
+        assert len(st.trace) == len(ref.trace) and st.nfe == ref.nfe
+        assert np.array_equal(got, ref.tokens)
+    assert np.all(got[Pl:] != shape.mask_id)
+    print(f"prefix cache {rule} k={k}: nfe {st.nfe}, first excluded step {excluded}")
