@@ -90,9 +90,30 @@ dllm_status check_stats(const dllm_stats* s, const char* name) {
 
 // Workspace layout of one forward (256-byte aligned regions).
 struct FwdLayout {
-  size_t x, a, q, k, vt, f, hl, lm, lmsrc, total;
+  size_t x, a, q, k, vt, f, hl, lm, lmsrc, part, total;
   int vt_ld;
 };
+
+// split-K parts of the four projections of a forward over M rows, and the
+// partial-tile workspace they share (one projection at a time)
+struct GemmSplits {
+  int qkv, o, gu, down;
+  size_t bytes;
+};
+
+GemmSplits plan_gemms(const dllm_model_desc& d, int M) {
+  const int dt = d.dtype;
+  auto cdiv = [](int a, int b) { return (a + b - 1) / b; };
+  const int tq = cdiv(3 * d.d_model, 256), to = cdiv(d.d_model, 256), tg = cdiv(d.d_ffn, 128);
+  GemmSplits g;
+  g.qkv = gemm_splits(M, tq, d.d_model, dt);
+  g.o = gemm_splits(M, to, d.d_model, dt);
+  g.gu = d.d_ffn % 4 ? 1 : gemm_splits(M, tg, d.d_model, dt);
+  g.down = gemm_splits(M, to, d.d_ffn, dt);
+  g.bytes = std::max(std::max(gemm_partial_bytes(M, tq, g.qkv), gemm_partial_bytes(M, to, g.o)),
+                     std::max(gemm_partial_bytes(M, tg, g.gu), gemm_partial_bytes(M, to, g.down)));
+  return g;
+}
 
 // packed lookahead layout of one forward (see dllm_forward_packed)
 struct Packing {
@@ -120,6 +141,7 @@ FwdLayout plan_forward(const dllm_model_desc& d, int batch, int seq, int R) {
   L.hl = take(size_t(R) * d.d_model * T);
   L.lm = take(lmhead_workspace(R, d.vocab));
   L.lmsrc = take(size_t(R) * 8);
+  L.part = take(plan_gemms(d, int(M)).bytes);
   L.total = off;
   return L;
 }
@@ -302,6 +324,12 @@ dllm_status forward_impl(dllm_model* m, const int32_t* tokens, int32_t batch, in
   void* hl = base + L.hl;
   const int dm = d.d_model, F = d.d_ffn, H = d.n_heads, hd = d.head_dim, dt = d.dtype;
   const int Mi = int(M);
+  const GemmSplits gs = plan_gemms(d, Mi);
+  float* part = reinterpret_cast<float*>(base + L.part);
+  // the residual projections leave their partials to the RMSNorm that follows
+  const SplitK sk_qkv{part, gs.qkv}, sk_o{part, gs.o, true}, sk_gu{part, gs.gu}, sk_down{part, gs.down, true};
+  const int np_d = (dm + 255) / 256 * 256;   // partial row pitch of the d-wide projections
+  int pending = 0;                            // split-K parts of x not yet added (0: none)
   // gathered row of each LM-head row (indexed modulo lm_n, per sequence) and
   // its row-scale index (its in-sequence position)
   const int32_t* lm_row = lm_pos;
@@ -321,11 +349,18 @@ dllm_status forward_impl(dllm_model* m, const int32_t* tokens, int32_t batch, in
     ProfScope ps(m, s, DLLM_PROF_EMBED);
     TRY_HIP(embed(dt, tokens, Mi, m->emb, dm, d.vocab, x, s), "embed");
   }
-  for (int l = 0; l < d.n_layers; ++l) {
-    {
-      ProfScope ps(m, s, DLLM_PROF_RMSNORM);
+  // a = rmsnorm(x), first adding the pending split-K partials of the last residual projection
+  auto norm_into_a = [&]() -> dllm_status {
+    ProfScope ps(m, s, DLLM_PROF_RMSNORM);
+    if (pending > 1)
+      TRY_HIP(resid_rmsnorm(dt, part, pending, np_d, Mi, x, dm, d.rms_eps, a, s), "resid_rmsnorm");
+    else
       TRY_HIP(rmsnorm(dt, x, dm, d.rms_eps, Mi, nullptr, 1, seq, a, s), "rmsnorm");
-    }
+    pending = 0;
+    return DLLM_OK;
+  };
+  for (int l = 0; l < d.n_layers; ++l) {
+    if (dllm_status e = norm_into_a(); e != DLLM_OK) return e;
     QkvOut qo{q, k, vt, seq, L.vt_ld, pos_offset, H, hd, dm, m->rope};
     if (pk) {
       qo.pack_S = pk->S;
@@ -334,7 +369,7 @@ dllm_status forward_impl(dllm_model* m, const int32_t* tokens, int32_t batch, in
     }
     {
       ProfScope ps(m, s, DLLM_PROF_GEMM_QKV);
-      TRY_HIP(gemm_qkv(dt, a, dm, m->wqkv[l], Mi, dm, qo, s), "gemm_qkv");
+      TRY_HIP(gemm_qkv(dt, a, dm, m->wqkv[l], Mi, dm, qo, s, &sk_qkv), "gemm_qkv");
     }
     if (kv_out) {
       const size_t lay = size_t(l) * H * kv_out->cap * hd * T;
@@ -371,20 +406,23 @@ dllm_status forward_impl(dllm_model* m, const int32_t* tokens, int32_t batch, in
     }
     {
       ProfScope ps(m, s, DLLM_PROF_GEMM_O);
-      TRY_HIP(gemm_resid(dt, a, dm, m->wo[l], dm, Mi, dm, dm, x, dm, s), "gemm_o");
+      TRY_HIP(gemm_resid(dt, a, dm, m->wo[l], dm, Mi, dm, dm, x, dm, s, &sk_o), "gemm_o");
+      pending = sk_o.splits;
     }
-    {
-      ProfScope ps(m, s, DLLM_PROF_RMSNORM);
-      TRY_HIP(rmsnorm(dt, x, dm, d.rms_eps, Mi, nullptr, 1, seq, a, s), "rmsnorm");
-    }
+    if (dllm_status e = norm_into_a(); e != DLLM_OK) return e;
     {
       ProfScope ps(m, s, DLLM_PROF_GEMM_GATEUP);
-      TRY_HIP(gemm_swiglu(dt, a, dm, m->wgu[l], Mi, F, dm, f, s), "gemm_swiglu");
+      TRY_HIP(gemm_swiglu(dt, a, dm, m->wgu[l], Mi, F, dm, f, s, &sk_gu), "gemm_swiglu");
     }
     {
       ProfScope ps(m, s, DLLM_PROF_GEMM_DOWN);
-      TRY_HIP(gemm_resid(dt, f, F, m->wdown[l], F, Mi, dm, F, x, dm, s), "gemm_down");
+      TRY_HIP(gemm_resid(dt, f, F, m->wdown[l], F, Mi, dm, F, x, dm, s, &sk_down), "gemm_down");
+      pending = sk_down.splits;
     }
+  }
+  if (pending > 1) {
+    ProfScope ps(m, s, DLLM_PROF_GEMM_DOWN);
+    TRY_HIP(splitk_add(sk_down, Mi, dm, x, dm, s), "split-K residual");
   }
   {
     ProfScope ps(m, s, DLLM_PROF_RMSNORM);

@@ -4,6 +4,13 @@
 //   qkv    : q, k, v = a Wqkv^T, rotary embedding on q and k, scattered to
 //            head-major Q/K and transposed V
 // 256x256 output tiles, 8 waves of 64x128, bf16 (or fp32) MFMA, fp32 accumulate.
+//
+// Few rows (a 512-row forward has 32 output tiles in the O and down
+// projections for 256 CUs): the K range is split into parts, every part
+// writes an fp32 partial tile to the workspace, and a reduction kernel adds
+// the parts in a fixed order (deterministic) and applies the epilogue.
+#include <algorithm>
+
 #include "kernels.h"
 #include "mainloop.h"
 
@@ -11,13 +18,26 @@ namespace dllm {
 
 namespace {
 
-constexpr int kBM = 256, kBN = 256;
-constexpr int kWavesM = 4, kWavesN = 2;   // 8 waves of 64 x 128, two per SIMD
-using Tile = TileMma<bf16_t, kBM, kBN, kWavesM, kWavesN>;  // geometry is the same for fp32
-constexpr int kThreads = Tile::kThreads;
+// Tile configurations, both with waves of 64 x 128 (the epilogues' layout):
+// Big 256 x 256 with 8 waves (two per SIMD, one workgroup per CU); Small
+// 64 x 256 with 2 waves for GEMMs of at most kSmallM rows, where a 256-row
+// tile would mostly multiply clamped duplicate rows (two workgroups per CU).
+template <int BM_, int BN_, int WM_, int WN_>
+struct GemmCfg {
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, kThreads = WM_ * WN_ * 64;
+};
+using Big = GemmCfg<256, 256, 4, 2>;
+using Small = GemmCfg<64, 256, 1, 2>;
+constexpr int kBN = 256;          // both configurations
 constexpr int kGroupM = 8;
+#ifndef DLLM_SMALL_M_MAX
+#define DLLM_SMALL_M_MAX 64
+#endif
+constexpr int kSmallM = DLLM_SMALL_M_MAX;
 
-enum { EPI_RESID = 0, EPI_SWIGLU = 1, EPI_QKV = 2 };
+// EPI_PART / EPI_PART_GU: split-K partial tiles (GU: the gate/up row pairing
+// of EPI_SWIGLU) written to part[split][M][np]
+enum { EPI_RESID = 0, EPI_SWIGLU = 1, EPI_QKV = 2, EPI_PART = 3, EPI_PART_GU = 4 };
 
 struct EpiParams {
   float* x;          // resid: fp32 residual
@@ -25,25 +45,37 @@ struct EpiParams {
   void* out;         // swiglu: [M][F]
   int F;
   QkvOut qkv;
+  float* part;       // split-K partials [splits][M][np]
+  int np;
 };
 
 // HD: head_dim of the QKV epilogue (compile-time, so the rotary partner block
 // index stays static and the accumulators stay in registers); 0 otherwise.
-template <typename T, int EPI, int HD>
-__global__ __launch_bounds__(kThreads, 2) void gemm_kernel(const T* __restrict__ A, int lda,
-                                                           const T* __restrict__ B, int ldb, int M, int N, int K,
-                                                           int tiles_m, int tiles_n, EpiParams ep) {
-  using TM = TileMma<T, kBM, kBN, kWavesM, kWavesN>;
+template <typename T, int EPI, int HD, class Cfg>
+__global__ __launch_bounds__(Cfg::kThreads, 2) void gemm_kernel(const T* __restrict__ A, int lda,
+                                                                const T* __restrict__ B, int ldb, int M, int N,
+                                                                int K, int tiles_m, int tiles_n, EpiParams ep) {
+  constexpr int kBM = Cfg::BM, kWavesN = Cfg::WN;
+  using TM = TileMma<T, Cfg::BM, Cfg::BN, Cfg::WM, Cfg::WN>;
+  constexpr bool kSplit = EPI == EPI_PART || EPI == EPI_PART_GU;
   __shared__ __attribute__((aligned(16))) uint8_t smem[TM::kSmem];
   int tm, tn;
   map_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, kGroupM, tm, tn);
   const int m0 = tm * kBM;
   const uint32_t a_row_bytes = uint32_t(lda) * sizeof(T);
   const uint32_t b_row_bytes = uint32_t(ldb) * sizeof(T);
-  auto a_off = [&](int r) -> uint32_t { return uint32_t(min(m0 + r, M - 1)) * a_row_bytes; };
+  // K stages of this part (128 bytes of every row per stage)
+  int st0 = 0, nst = K / (2 * TM::kKPerStage);
+  if constexpr (kSplit) {
+    const int all = nst, split = blockIdx.y;
+    st0 = split * all / int(gridDim.y);
+    nst = (split + 1) * all / int(gridDim.y) - st0;
+  }
+  const uint32_t k_bytes = uint32_t(st0) * TM::kRowBytes;
+  auto a_off = [&](int r) -> uint32_t { return uint32_t(min(m0 + r, M - 1)) * a_row_bytes + k_bytes; };
   auto b_off = [&](int r) -> uint32_t {
     int row;
-    if constexpr (EPI == EPI_SWIGLU) {
+    if constexpr (EPI == EPI_SWIGLU || EPI == EPI_PART_GU) {
       // 256 B rows -> 128 outputs: each 128-row half of a wave column pairs 64 gate and 64 up rows
       const int wn = r >> 7, rr = r & 127;
       const int j = min(tn * 128 + wn * 64 + (rr & 63), ep.F - 1);
@@ -51,18 +83,47 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(const T* __restrict__
     } else {
       row = min(tn * kBN + r, N - 1);
     }
-    return uint32_t(row) * b_row_bytes;
+    return uint32_t(row) * b_row_bytes + k_bytes;
   };
   f32x4 acc[TM::kFM][TM::kFN];
-  TM::run(smem, reinterpret_cast<const uint8_t*>(A), reinterpret_cast<const uint8_t*>(B), a_off, b_off,
-          K / TM::kKPerStage, acc);
+  TM::run(smem, reinterpret_cast<const uint8_t*>(A), reinterpret_cast<const uint8_t*>(B), a_off, b_off, 2 * nst,
+          acc);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / kWavesN, wn = wave % kWavesN;
   const int row_base = m0 + wm * TM::kWTM + 4 * (lane >> 4);
   const int lc = lane & 15;
 
-  if constexpr (EPI == EPI_RESID) {
+  if constexpr (kSplit) {
+    // the fp32 partial tile through LDS as in the residual epilogue, 16-byte
+    // stores along rows of part[split]
+    static_assert(TM::kWTM == 64 && TM::kWTN == 128, "partial epilogue tiling");
+    uint8_t* st = smem + wave * (64 * 64 * 4);
+    auto slot_of = [](int r, int c4) { return r * 256 + (((c4 ^ (r & 15))) << 4); };
+    const int r0 = m0 + wm * 64;
+    float* P = ep.part + size_t(blockIdx.y) * M * ep.np;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+      for (int m = 0; m < TM::kFM; ++m)
+#pragma unroll
+        for (int nn = 0; nn < 4; ++nn)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int r = m * 16 + 4 * (lane >> 4) + i, c = nn * 16 + lc;
+            *reinterpret_cast<float*>(st + slot_of(r, c >> 2) + (c & 3) * 4) = acc[m][4 * h + nn][i];
+          }
+      const int c0 = tn * kBN + wn * TM::kWTN + 64 * h;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int q = lane + 64 * j, r = q >> 4, c4 = q & 15;
+        const int row = r0 + r;
+        if (row < M)
+          *reinterpret_cast<f32x4*>(P + size_t(row) * ep.np + c0 + 4 * c4) =
+              *reinterpret_cast<const f32x4*>(st + slot_of(r, c4));
+      }
+    }
+  } else if constexpr (EPI == EPI_RESID) {
     // x += acc through LDS: each wave stages half of its 64 x 128 tile at a
     // time (64 x 64 fp32, 16 KB, in its own region of the idle ring), rows of
     // 16 chunks of 4 floats with chunk c of row r in slot c ^ (r % 16), so
@@ -233,43 +294,258 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(const T* __restrict__
   }
 }
 
+template <typename T, int EPI, int HD, class Cfg>
+hipError_t launch_cfg(const void* A, int lda, const void* B, int ldb, int M, int N, int K, int tiles_n,
+                      const EpiParams& ep, hipStream_t s, int splits) {
+  // the mainloop runs stages in pairs
+  constexpr int kStageK = 2 * TileMma<T, Cfg::BM, Cfg::BN, Cfg::WM, Cfg::WN>::kKPerStage;
+  if (K <= 0 || K % kStageK || splits < 1 || splits > K / kStageK) return hipErrorInvalidValue;
+  const int tiles_m = cdiv(M, Cfg::BM);
+  const int grid = tiles_m * tiles_n;
+  hipLaunchKernelGGL((gemm_kernel<T, EPI, HD, Cfg>), dim3(grid, splits), dim3(Cfg::kThreads), 0, s,
+                     static_cast<const T*>(A), lda, static_cast<const T*>(B), ldb, M, N, K, tiles_m, tiles_n, ep);
+  return hipGetLastError();
+}
+
 template <typename T, int EPI, int HD = 0>
 hipError_t launch(const void* A, int lda, const void* B, int ldb, int M, int N, int K, int tiles_n,
-                  const EpiParams& ep, hipStream_t s) {
-  // the mainloop runs stages in pairs
-  if (K <= 0 || K % (2 * TileMma<T, kBM, kBN, kWavesM, kWavesN>::kKPerStage)) return hipErrorInvalidValue;
-  const int tiles_m = cdiv(M, kBM);
-  const int grid = tiles_m * tiles_n;
-  hipLaunchKernelGGL((gemm_kernel<T, EPI, HD>), dim3(grid), dim3(kThreads), 0, s, static_cast<const T*>(A), lda,
-                     static_cast<const T*>(B), ldb, M, N, K, tiles_m, tiles_n, ep);
-  return hipGetLastError();
+                  const EpiParams& ep, hipStream_t s, int splits = 1) {
+  return M <= kSmallM ? launch_cfg<T, EPI, HD, Small>(A, lda, B, ldb, M, N, K, tiles_n, ep, s, splits)
+                      : launch_cfg<T, EPI, HD, Big>(A, lda, B, ldb, M, N, K, tiles_n, ep, s, splits);
+}
+
+// ---------------------------------------------------------------- split-K reductions
+
+constexpr int kRedThreads = 256;
+
+// x[row][c..c+3] += part[0] + part[1] + ... (in this order)
+__global__ __launch_bounds__(kRedThreads) void splitk_resid_kernel(const float* __restrict__ part, int splits,
+                                                                   int M, int N, int np, float* __restrict__ x,
+                                                                   int ldx) {
+  const int n4 = N >> 2;
+  const int i = blockIdx.x * kRedThreads + threadIdx.x;
+  if (i >= M * n4) return;
+  const int row = i / n4, c = (i - row * n4) * 4;
+  f32x4 acc = *reinterpret_cast<const f32x4*>(x + size_t(row) * ldx + c);
+  auto pr = [&](int p) { return *reinterpret_cast<const f32x4*>(part + (size_t(p) * M + row) * np + c); };
+  int p = 0;
+  for (; p + 4 <= splits; p += 4) {   // four loads in flight, added in order
+    const f32x4 a0 = pr(p), a1 = pr(p + 1), a2 = pr(p + 2), a3 = pr(p + 3);
+    acc += a0;
+    acc += a1;
+    acc += a2;
+    acc += a3;
+  }
+  for (; p < splits; ++p) acc += pr(p);
+  *reinterpret_cast<f32x4*>(x + size_t(row) * ldx + c) = acc;
+}
+
+// out[row][j..j+3] = silu(g) * u; gate j sits at partial column
+// (j / 128) * 256 + ((j % 128) / 64) * 128 + j % 64, its up partner 64 further
+template <typename T>
+__global__ __launch_bounds__(kRedThreads) void splitk_swiglu_kernel(const float* __restrict__ part, int splits,
+                                                                    int M, int F, int np, T* __restrict__ out) {
+  const int f4 = F >> 2;
+  const int i = blockIdx.x * kRedThreads + threadIdx.x;
+  if (i >= M * f4) return;
+  const int row = i / f4, j = (i - row * f4) * 4;
+  const int gc = (j >> 7) * 256 + ((j & 127) >> 6) * 128 + (j & 63);
+  f32x4 g = f32x4{0.f, 0.f, 0.f, 0.f}, u = g;
+  const float* src = part + size_t(row) * np + gc;
+  const size_t stride = size_t(M) * np;
+  int p = 0;
+  for (; p + 2 <= splits; p += 2) {
+    const f32x4 g0 = *reinterpret_cast<const f32x4*>(src + p * stride),
+                u0 = *reinterpret_cast<const f32x4*>(src + p * stride + 64),
+                g1 = *reinterpret_cast<const f32x4*>(src + (p + 1) * stride),
+                u1 = *reinterpret_cast<const f32x4*>(src + (p + 1) * stride + 64);
+    g += g0;
+    u += u0;
+    g += g1;
+    u += u1;
+  }
+  for (; p < splits; ++p) {
+    g += *reinterpret_cast<const f32x4*>(src + p * stride);
+    u += *reinterpret_cast<const f32x4*>(src + p * stride + 64);
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) store_f(out + size_t(row) * F + j + e, g[e] / (1.0f + __expf(-g[e])) * u[e]);
+}
+
+// in-sequence position id of row `row` of the QKV projection (as the fused epilogue)
+__device__ __forceinline__ int qkv_pos(const QkvOut& o, int row) {
+  const int r = row % o.seq;
+  return o.pos_offset + (o.pack_B && r >= o.pack_S ? o.pack_b0 + ((r - o.pack_S) & (o.pack_B - 1)) : r);
+}
+
+// Q and K: one thread per (row, q or k, head, dim < HD/2) pair; sums the two
+// partners, rotates them and writes both to the head-major layout
+template <typename T, int HD>
+__global__ __launch_bounds__(kRedThreads) void splitk_qk_kernel(const float* __restrict__ part, int splits, int M,
+                                                                int np, QkvOut o) {
+  constexpr int half = HD / 2;
+  const int d = o.d;
+  const int i = blockIdx.x * kRedThreads + threadIdx.x;
+  if (i >= M * d) return;
+  const int row = i / d, p = i - row * d;
+  const int which = p / (d / 2), rest = p - which * (d / 2);
+  const int h = rest / half, dim = rest - h * half;
+  const int c1 = which * d + h * HD + dim;
+  float x1 = 0.f, x2 = 0.f;
+  const float* src = part + size_t(row) * np + c1;
+  const size_t stride = size_t(M) * np;
+  int s = 0;
+  for (; s + 2 <= splits; s += 2) {
+    const float a0 = src[s * stride], b0 = src[s * stride + half], a1 = src[(s + 1) * stride],
+                b1 = src[(s + 1) * stride + half];
+    x1 += a0;
+    x2 += b0;
+    x1 += a1;
+    x2 += b1;
+  }
+  for (; s < splits; ++s) {
+    x1 += src[s * stride];
+    x2 += src[s * stride + half];
+  }
+  const float2 cs = o.rope[size_t(qkv_pos(o, row)) * half + dim];
+  const int b = row / o.seq, sp = row - b * o.seq;
+  T* dst = static_cast<T*>(which == 0 ? o.q : o.k) + (size_t(b * o.H + h) * o.seq + sp) * HD;
+  store_f(dst + dim, x1 * cs.x - x2 * cs.y);
+  store_f(dst + dim + half, x1 * cs.y + x2 * cs.x);
+}
+
+// V: 16-row x 64-column tiles transposed through LDS so that both the partial
+// reads (along columns) and the V^T writes (along positions) are contiguous
+template <typename T>
+__global__ __launch_bounds__(kRedThreads) void splitk_v_kernel(const float* __restrict__ part, int splits, int M,
+                                                               int np, QkvOut o) {
+  __shared__ float tile[16][65];
+  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 16, d = o.d;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int idx = threadIdx.x + kRedThreads * e, r = idx >> 6, c = idx & 63, row = r0 + r, col = c0 + c;
+    float v = 0.f;
+    if (row < M && col < d) {
+      const float* src = part + size_t(row) * np + 2 * d + col;
+      const size_t stride = size_t(M) * np;
+      int p = 0;
+      for (; p + 4 <= splits; p += 4) {
+        const float a0 = src[p * stride], a1 = src[(p + 1) * stride], a2 = src[(p + 2) * stride],
+                    a3 = src[(p + 3) * stride];
+        v += a0;
+        v += a1;
+        v += a2;
+        v += a3;
+      }
+      for (; p < splits; ++p) v += src[p * stride];
+    }
+    tile[r][c] = v;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int idx = threadIdx.x + kRedThreads * e, c = idx >> 4, r = idx & 15, row = r0 + r, col = c0 + c;
+    if (row >= M || col >= d) continue;
+    const int b = row / o.seq, sp = row - b * o.seq, h = col / o.hd, dim = col - h * o.hd;
+    store_f(static_cast<T*>(o.vt) + (size_t(b * o.H + h) * o.hd + dim) * o.vt_ld + sp, tile[r][c]);
+  }
 }
 
 }  // namespace
 
+hipError_t splitk_add(const SplitK& sk, int M, int N, float* X, int ldx, hipStream_t s) {
+  if (N % 4 || ldx % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(splitk_resid_kernel, dim3(cdiv(M * (N / 4), kRedThreads)), dim3(kRedThreads), 0, s, sk.part,
+                     sk.splits, M, N, cdiv(N, kBN) * kBN, X, ldx);
+  return hipGetLastError();
+}
+
+int gemm_splits(int M, int tiles_n, int K, int dtype) {
+  // workgroups that fill the 256 CUs: one 256-row workgroup per CU, two small ones
+  const bool small = M <= kSmallM;
+  const int tiles = cdiv(M, small ? Small::BM : Big::BM) * tiles_n, full = small ? 512 : 256;
+  const int stages = K / (dtype ? 64 : 32);   // 128-byte K stages
+  if (tiles >= full * 5 / 8 || stages < 2) return 1;
+  return std::max(1, std::min(full / tiles, stages / 4));
+}
+
+size_t gemm_partial_bytes(int M, int tiles_n, int splits) {
+  return splits > 1 ? size_t(splits) * M * tiles_n * kBN * sizeof(float) : 0;
+}
+
 hipError_t gemm_resid(int dtype, const void* A, int lda, const void* B, int ldb, int M, int N, int K, float* X,
-                      int ldx, hipStream_t s) {
+                      int ldx, hipStream_t s, const SplitK* sk) {
   if (N % 4 || ldx % 4 || reinterpret_cast<uintptr_t>(X) % 16) return hipErrorInvalidValue;   // 16-byte x accesses
   EpiParams ep{};
   ep.x = X;
   ep.ldx = ldx;
   const int tn = cdiv(N, kBN);
+  if (sk && sk->splits > 1) {
+    ep.part = sk->part;
+    ep.np = tn * kBN;
+    hipError_t e = dtype ? launch<bf16_t, EPI_PART>(A, lda, B, ldb, M, N, K, tn, ep, s, sk->splits)
+                         : launch<float, EPI_PART>(A, lda, B, ldb, M, N, K, tn, ep, s, sk->splits);
+    if (e != hipSuccess || sk->defer) return e;
+    return splitk_add(*sk, M, N, X, ldx, s);
+  }
   return dtype ? launch<bf16_t, EPI_RESID>(A, lda, B, ldb, M, N, K, tn, ep, s)
                : launch<float, EPI_RESID>(A, lda, B, ldb, M, N, K, tn, ep, s);
 }
 
 hipError_t gemm_swiglu(int dtype, const void* A, int lda, const void* Wgu, int M, int F, int K, void* out,
-                       hipStream_t s) {
+                       hipStream_t s, const SplitK* sk) {
   EpiParams ep{};
   ep.out = out;
   ep.F = F;
   const int tn = cdiv(F, 128);
+  if (sk && sk->splits > 1) {
+    if (F % 4) return hipErrorInvalidValue;
+    ep.part = sk->part;
+    ep.np = tn * kBN;
+    hipError_t e = dtype ? launch<bf16_t, EPI_PART_GU>(A, lda, Wgu, K, M, 2 * F, K, tn, ep, s, sk->splits)
+                         : launch<float, EPI_PART_GU>(A, lda, Wgu, K, M, 2 * F, K, tn, ep, s, sk->splits);
+    if (e != hipSuccess) return e;
+    const dim3 g(cdiv(M * (F / 4), kRedThreads));
+    if (dtype)
+      hipLaunchKernelGGL(splitk_swiglu_kernel<bf16_t>, g, dim3(kRedThreads), 0, s, sk->part, sk->splits, M, F, ep.np,
+                         static_cast<bf16_t*>(out));
+    else
+      hipLaunchKernelGGL(splitk_swiglu_kernel<float>, g, dim3(kRedThreads), 0, s, sk->part, sk->splits, M, F, ep.np,
+                         static_cast<float*>(out));
+    return hipGetLastError();
+  }
   return dtype ? launch<bf16_t, EPI_SWIGLU>(A, lda, Wgu, K, M, 2 * F, K, tn, ep, s)
                : launch<float, EPI_SWIGLU>(A, lda, Wgu, K, M, 2 * F, K, tn, ep, s);
 }
 
+namespace {
+
+template <typename T>
+hipError_t qkv_split(const void* A, int lda, const void* Wqkv, int M, int K, const QkvOut& o, hipStream_t s,
+                     const SplitK& sk) {
+  EpiParams ep{};
+  ep.qkv = o;
+  const int N = 3 * o.d, tn = cdiv(N, kBN);
+  ep.part = sk.part;
+  ep.np = tn * kBN;
+  hipError_t e = launch<T, EPI_PART>(A, lda, Wqkv, K, M, N, K, tn, ep, s, sk.splits);
+  if (e != hipSuccess) return e;
+  const dim3 g(cdiv(M * o.d, kRedThreads));
+  if (o.hd == 128)
+    hipLaunchKernelGGL((splitk_qk_kernel<T, 128>), g, dim3(kRedThreads), 0, s, sk.part, sk.splits, M, ep.np, o);
+  else
+    hipLaunchKernelGGL((splitk_qk_kernel<T, 64>), g, dim3(kRedThreads), 0, s, sk.part, sk.splits, M, ep.np, o);
+  hipLaunchKernelGGL(splitk_v_kernel<T>, dim3(cdiv(o.d, 64), cdiv(M, 16)), dim3(kRedThreads), 0, s, sk.part,
+                     sk.splits, M, ep.np, o);
+  return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t gemm_qkv(int dtype, const void* A, int lda, const void* Wqkv, int M, int K, const QkvOut& o,
-                    hipStream_t s) {
+                    hipStream_t s, const SplitK* sk) {
+  if (sk && sk->splits > 1)
+    return dtype ? qkv_split<bf16_t>(A, lda, Wqkv, M, K, o, s, *sk) : qkv_split<float>(A, lda, Wqkv, M, K, o, s, *sk);
   EpiParams ep{};
   ep.qkv = o;
   const int N = 3 * o.d;

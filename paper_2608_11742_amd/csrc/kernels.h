@@ -22,15 +22,34 @@ struct QkvOut {
   int pack_S = 0, pack_b0 = 0, pack_B = 0;
 };
 
+// Split-K of a projection GEMM with few rows: `splits` parts of the K range
+// write fp32 partial tiles to `part` (gemm_partial_bytes), reduced in a fixed
+// order by a second kernel that applies the epilogue.  splits <= 1: one pass.
+struct SplitK {
+  float* part;
+  int splits;
+  bool defer = false;   // resid: write the partials only; the caller adds them (resid_rmsnorm / splitk_add)
+};
+// parts for M rows, tiles_n 256-wide column tiles (gate/up: F / 128) and K
+int gemm_splits(int M, int tiles_n, int K, int dtype);
+size_t gemm_partial_bytes(int M, int tiles_n, int splits);
+
 // X[M][N] (fp32, row stride ldx) += A[M][K] B[N][K]^T
 hipError_t gemm_resid(int dtype, const void* A, int lda, const void* B, int ldb, int M, int N, int K, float* X,
-                      int ldx, hipStream_t s);
+                      int ldx, hipStream_t s, const SplitK* sk = nullptr);
 // out[M][F] = silu(A Wg^T) * (A Wu^T) with Wgu = [Wg; Wu] ([2F][K])
 hipError_t gemm_swiglu(int dtype, const void* A, int lda, const void* Wgu, int M, int F, int K, void* out,
-                       hipStream_t s);
+                       hipStream_t s, const SplitK* sk = nullptr);
 // Q/K/V projection with rotary embedding on Q and K, scattered head-major
 hipError_t gemm_qkv(int dtype, const void* A, int lda, const void* Wqkv, int M, int K, const QkvOut& o,
-                    hipStream_t s);
+                    hipStream_t s, const SplitK* sk = nullptr);
+
+// x[M][N] += the deferred split-K partials of gemm_resid (fixed order)
+hipError_t splitk_add(const SplitK& sk, int M, int N, float* X, int ldx, hipStream_t s);
+// x[r] += the deferred split-K partials of gemm_resid (row pitch np), then
+// out[r] = rmsnorm(x[r]), for rows 0 .. M-1
+hipError_t resid_rmsnorm(int dtype, const float* part, int splits, int np, int M, float* x, int d, float eps,
+                         void* out, hipStream_t s);
 
 // x[r][:] = emb[tok[r]][:] as fp32
 hipError_t embed(int dtype, const int32_t* tok, int rows, const void* emb, int d, int vocab, float* x, hipStream_t s);

@@ -8,7 +8,7 @@
 // 4 threads per row scan 64 logits each, updating a running max m,
 // s = sum exp(l - m), t = sum exp(l - m) (l - m) and a sorted top-16 held in
 // registers.  At the end of its slice every thread writes its partial state.
-// Pass 2 (merge_kernel): one wave per row merges all partials:
+// Pass 2 (merge_kernel): one workgroup per row merges all partials:
 //   M = max m_p, S = sum s_p e^(m_p - M), T = sum e^(m_p - M) (t_p + (m_p - M) s_p)
 //   lse = M + log S, H = log S - T / S, lmax = M,
 // and a 64-way merge of the sorted partial top-16 lists.
@@ -263,21 +263,34 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_kernel(const T* __restrict
   }
 }
 
-// One wave per row.
-__global__ __launch_bounds__(256) void merge_kernel(Partials part, int R, StatsOut out) {
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
+// One workgroup of W = blockDim.x / 64 waves per row (W grows with the number
+// of partials, so that rows with many vocabulary slices merge in parallel).
+// Every lane folds a strided share of the row's partials into (S, T) and a
+// sorted top-16; each wave merges its lanes' lists into its own top-16 by
+// repeated wave-wide argmax; the waves' lists and sums meet in LDS and wave 0
+// merges them the same way.
+__global__ __launch_bounds__(512) void merge_kernel(Partials part, int R, StatsOut out) {
+  constexpr int kMaxW = 8;
+  __shared__ float red_m[kMaxW], red_s[kMaxW], red_t[kMaxW];
+  __shared__ float lv[kMaxW][kK];
+  __shared__ int li[kMaxW][kK];
+  const int row = blockIdx.x;
+  const int W = blockDim.x >> 6, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   if (row >= R) return;
   const size_t base = size_t(row) * part.P;
   float M = -INFINITY;
-  for (int p = lane; p < part.P; p += 64) M = fmaxf(M, part.m[base + p]);
+  for (int p = threadIdx.x; p < part.P; p += blockDim.x) M = fmaxf(M, part.m[base + p]);
   M = wave_max(M);
+  if (lane == 0) red_m[wave] = M;
+  __syncthreads();
+  M = red_m[0];
+  for (int w = 1; w < W; ++w) M = fmaxf(M, red_m[w]);
   float S = 0.f, Tt = 0.f;
   float tv[kK];
   int ti[kK];
 #pragma unroll
   for (int k = 0; k < kK; ++k) { tv[k] = -INFINITY; ti[k] = 0x7fffffff; }
-  for (int p = lane; p < part.P; p += 64) {
+  for (int p = threadIdx.x; p < part.P; p += blockDim.x) {
     const float mp = part.m[base + p];
     if (mp == -INFINITY) continue;  // a partial that saw no valid logit
     const float w = fast_exp(mp - M);
@@ -295,23 +308,44 @@ __global__ __launch_bounds__(256) void merge_kernel(Partials part, int R, StatsO
   }
   S = wave_sum(S);
   Tt = wave_sum(Tt);
-  // 64-way merge of the lanes' sorted lists: the wave-wide best head is taken K times
-  for (int k = 0; k < out.k; ++k) {
-    float v = tv[0];
-    int i = ti[0];
-    wave_argmax(v, i);
+  // 64-way merge of the lanes' sorted lists: the wave-wide best head is taken n times
+  auto merge_lanes = [&](int n, auto&& emit) {
+    for (int k = 0; k < n; ++k) {
+      float v = tv[0];
+      int i = ti[0];
+      wave_argmax(v, i);
+      emit(k, v, i);
+      if (ti[0] == i) {  // ids are unique: exactly one lane owns the winner; pop it
+#pragma unroll
+        for (int j = 0; j < kK - 1; ++j) { tv[j] = tv[j + 1]; ti[j] = ti[j + 1]; }
+        tv[kK - 1] = -INFINITY;
+        ti[kK - 1] = 0x7fffffff;
+      }
+    }
+  };
+  if (W > 1) {
+    merge_lanes(kK, [&](int k, float v, int i) {
+      if (lane == 0) { lv[wave][k] = v; li[wave][k] = i; }
+    });
+    if (lane == 0) { red_s[wave] = S; red_t[wave] = Tt; }
+    __syncthreads();
+    if (wave != 0) return;
+    S = red_s[0];
+    Tt = red_t[0];
+    for (int w = 1; w < W; ++w) { S += red_s[w]; Tt += red_t[w]; }
+#pragma unroll
+    for (int k = 0; k < kK; ++k) {
+      tv[k] = lane < W ? lv[lane][k] : -INFINITY;
+      ti[k] = lane < W ? li[lane][k] : 0x7fffffff;
+    }
+  }
+  merge_lanes(out.k, [&](int k, float v, int i) {
     if (lane == 0) {
       out.topk_id[size_t(row) * out.k + k] = i;
       out.topk_logit[size_t(row) * out.k + k] = v;
+      if (k == 0) out.argmax[row] = i;
     }
-    if (ti[0] == i) {  // ids are unique: exactly one lane owns the winner; pop it
-#pragma unroll
-      for (int j = 0; j < kK - 1; ++j) { tv[j] = tv[j + 1]; ti[j] = ti[j + 1]; }
-      tv[kK - 1] = -INFINITY;
-      ti[kK - 1] = 0x7fffffff;
-    }
-    if (k == 0 && lane == 0) out.argmax[row] = i;
-  }
+  });
   if (lane == 0) {
     const float logS = logf(S);
     out.lmax[row] = M;
@@ -392,7 +426,8 @@ hipError_t lmhead_partials(int dtype, const void* h, const void* w, int R, int d
 
 hipError_t lmhead_merge(int R, int V, const StatsOut& out, void* ws, hipStream_t s) {
   Partials part = carve(ws, R, partials_per_row(R, V));
-  hipLaunchKernelGGL(merge_kernel, dim3(cdiv(R, 4)), dim3(256), 0, s, part, R, out);
+  const int waves = std::min(8, std::max(1, cdiv(part.P, 128)));
+  hipLaunchKernelGGL(merge_kernel, dim3(R), dim3(64 * waves), 0, s, part, R, out);
   return hipGetLastError();
 }
 

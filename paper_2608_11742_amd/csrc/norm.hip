@@ -51,6 +51,49 @@ __global__ __launch_bounds__(kRowThreads) void rmsnorm_kernel(const float* __res
   }
 }
 
+// Residual update from split-K partial tiles fused with the RMSNorm that
+// follows it: x[r] += part[0][r] + part[1][r] + ... (in this order, as the
+// separate reduction), then out[r] = x[r] / sqrt(mean(x[r]^2) + eps).
+template <typename T>
+__global__ __launch_bounds__(kRowThreads) void resid_rmsnorm_kernel(const float* __restrict__ part, int splits,
+                                                                    int np, int M, float* __restrict__ x, int d,
+                                                                    float eps, T* __restrict__ out) {
+  __shared__ float red[kRowThreads / kWave];
+  const int r = blockIdx.x;
+  float* xr = x + size_t(r) * d;
+  auto pr = [&](int p, int c) { return *reinterpret_cast<const f32x4*>(part + (size_t(p) * M + r) * np + c); };
+  float ss = 0.f;
+  for (int c = threadIdx.x * 4; c < d; c += kRowThreads * 4) {
+    f32x4 v = *reinterpret_cast<const f32x4*>(xr + c);
+    int p = 0;
+    for (; p + 4 <= splits; p += 4) {   // four loads in flight, added in order
+      const f32x4 a0 = pr(p, c), a1 = pr(p + 1, c), a2 = pr(p + 2, c), a3 = pr(p + 3, c);
+      v += a0;
+      v += a1;
+      v += a2;
+      v += a3;
+    }
+    for (; p < splits; ++p) v += pr(p, c);
+    *reinterpret_cast<f32x4*>(xr + c) = v;
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < kRowThreads / kWave; ++w) tot += red[w];
+  const float inv = 1.0f / sqrtf(tot / float(d) + eps);
+  T* o = out + size_t(r) * d;
+  for (int c = threadIdx.x * 4; c < d; c += kRowThreads * 4) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(xr + c);   // this thread's own writes
+    store_f(o + c + 0, v.x * inv);
+    store_f(o + c + 1, v.y * inv);
+    store_f(o + c + 2, v.z * inv);
+    store_f(o + c + 3, v.w * inv);
+  }
+}
+
 // grid: (H, rows of this call); copies K rows and V^T columns into the cache
 template <typename T>
 __global__ __launch_bounds__(kRowThreads) void kv_store_kernel(const T* __restrict__ k, const T* __restrict__ vt,
@@ -82,6 +125,18 @@ hipError_t rmsnorm(int dtype, const float* x, int d, float eps, int rows, const 
                        static_cast<bf16_t*>(out));
   else
     hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(rows), dim3(kRowThreads), 0, s, x, d, eps, pos, n_pos, seq,
+                       static_cast<float*>(out));
+  return hipGetLastError();
+}
+
+hipError_t resid_rmsnorm(int dtype, const float* part, int splits, int np, int M, float* x, int d, float eps,
+                         void* out, hipStream_t s) {
+  if (d % 4 || np % 4) return hipErrorInvalidValue;
+  if (dtype)
+    hipLaunchKernelGGL(resid_rmsnorm_kernel<bf16_t>, dim3(M), dim3(kRowThreads), 0, s, part, splits, np, M, x, d, eps,
+                       static_cast<bf16_t*>(out));
+  else
+    hipLaunchKernelGGL(resid_rmsnorm_kernel<float>, dim3(M), dim3(kRowThreads), 0, s, part, splits, np, M, x, d, eps,
                        static_cast<float*>(out));
   return hipGetLastError();
 }

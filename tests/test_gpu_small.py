@@ -118,6 +118,21 @@ def test_forward_small_bf16_against_mirror(P, small_bf16):
     print(compare_stats(out.numpy(), ref, 2e-2, margin="auto", label="forward small bf16"))
 
 
+@pytest.mark.parametrize("S", [40, 64])
+def test_forward_small_bf16_few_rows(P, small_bf16, S):
+    """Few-row forwards (the 64-row GEMM tiles and split-K reductions of a
+    block forward) against the mirror oracle."""
+    shape, w_np, model = small_bf16
+    toks = synth.tokens_np(15 + S, "toks", S, shape.vocab - 1)
+    toks[S // 2:] = shape.mask_id
+    lm_pos = np.arange(S // 2, S, dtype=np.int32)
+    out = model.forward(torch.from_numpy(toks).to(DEV)[None], torch.from_numpy(lm_pos).to(DEV), scale=3.0)
+    torch.cuda.synchronize()
+    logits = om.forward_logits(toks[None], w_np, shape, lm_pos, scale=3.0, mirror=True)
+    ref = softmax_stats(logits.reshape(-1, shape.vocab), 16)
+    print(compare_stats(out.numpy(), ref, 2e-2, margin="auto", label=f"forward small bf16 1x{S}"))
+
+
 def test_cached_prefix_forward_tiny(P, tiny):
     shape, w_np, model = tiny
     Pn, Bk, nb = 40, 24, 3
