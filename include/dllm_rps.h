@@ -64,7 +64,7 @@ typedef void* dllm_stream;  /* hipStream_t */
  * bidirectional pre-RMSNorm transformer with rotate-half RoPE, full
  * non-causal softmax attention, SwiGLU feed-forward, untied embedding and LM
  * head, unit RMSNorm gains and no biases.  Requirements: d_model =
- * n_heads * head_dim, head_dim in {64, 128}, d_model % 256 == 0,
+ * n_heads * head_dim, head_dim in {64, 128}, d_model % 256 == 0, d_model <= 8192,
  * d_ffn % 128 == 0, 0 <= mask_id < vocab. */
 typedef struct {
     int32_t n_layers, d_model, n_heads, head_dim, d_ffn, vocab, mask_id;

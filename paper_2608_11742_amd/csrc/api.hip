@@ -176,7 +176,7 @@ dllm_status dllm_model_create(const dllm_model_desc* desc, const dllm_weights* w
     return fail(DLLM_ESHAPE, "non-positive model size");
   if (d.head_dim != 64 && d.head_dim != 128) return fail(DLLM_ESHAPE, "head_dim %d not in {64, 128}", d.head_dim);
   if (d.d_model != d.n_heads * d.head_dim) return fail(DLLM_ESHAPE, "d_model != n_heads * head_dim");
-  if (d.d_model % 256) return fail(DLLM_ESHAPE, "d_model %% 256 != 0");
+  if (d.d_model % 256 || d.d_model > 8192) return fail(DLLM_ESHAPE, "d_model %% 256 != 0 or d_model > 8192");
   if (d.d_ffn % 128) return fail(DLLM_ESHAPE, "d_ffn %% 128 != 0");
   if (d.mask_id < 0 || d.mask_id >= d.vocab) return fail(DLLM_EINVAL, "mask_id outside [0, vocab)");
   if (!(d.rms_eps > 0.f) || !(d.rope_base > 1.f)) return fail(DLLM_EINVAL, "rms_eps / rope_base");

@@ -22,12 +22,12 @@ namespace {
 // Big 256 x 256 with 8 waves (two per SIMD, one workgroup per CU); Small
 // 64 x 256 with 2 waves for GEMMs of at most kSmallM rows, where a 256-row
 // tile would mostly multiply clamped duplicate rows (two workgroups per CU).
-template <int BM_, int BN_, int WM_, int WN_>
+template <int BM_, int BN_, int WM_, int WN_, int MIN_BLOCKS>
 struct GemmCfg {
-  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, kThreads = WM_ * WN_ * 64;
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, kThreads = WM_ * WN_ * 64, kMinBlocks = MIN_BLOCKS;
 };
-using Big = GemmCfg<256, 256, 4, 2>;
-using Small = GemmCfg<64, 256, 1, 2>;
+using Big = GemmCfg<256, 256, 4, 2, 2>;
+using Small = GemmCfg<64, 256, 1, 2, 2>;
 constexpr int kBN = 256;          // both configurations
 constexpr int kGroupM = 8;
 #ifndef DLLM_SMALL_M_MAX
@@ -52,7 +52,7 @@ struct EpiParams {
 // HD: head_dim of the QKV epilogue (compile-time, so the rotary partner block
 // index stays static and the accumulators stay in registers); 0 otherwise.
 template <typename T, int EPI, int HD, class Cfg>
-__global__ __launch_bounds__(Cfg::kThreads, 2) void gemm_kernel(const T* __restrict__ A, int lda,
+__global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(const T* __restrict__ A, int lda,
                                                                 const T* __restrict__ B, int ldb, int M, int N,
                                                                 int K, int tiles_m, int tiles_n, EpiParams ep) {
   constexpr int kBM = Cfg::BM, kWavesN = Cfg::WN;
@@ -97,30 +97,33 @@ __global__ __launch_bounds__(Cfg::kThreads, 2) void gemm_kernel(const T* __restr
   if constexpr (kSplit) {
     // the fp32 partial tile through LDS as in the residual epilogue, 16-byte
     // stores along rows of part[split]
-    static_assert(TM::kWTM == 64 && TM::kWTN == 128, "partial epilogue tiling");
+    static_assert(TM::kWTM % 64 == 0 && TM::kWTN == 128, "partial epilogue tiling");
     uint8_t* st = smem + wave * (64 * 64 * 4);
     auto slot_of = [](int r, int c4) { return r * 256 + (((c4 ^ (r & 15))) << 4); };
-    const int r0 = m0 + wm * 64;
     float* P = ep.part + size_t(blockIdx.y) * M * ep.np;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int g = 0; g < TM::kWTM / 64; ++g) {   // 64-row groups of the wave tile
+      const int r0 = m0 + wm * TM::kWTM + 64 * g;
 #pragma unroll
-      for (int m = 0; m < TM::kFM; ++m)
+      for (int h = 0; h < 2; ++h) {
 #pragma unroll
-        for (int nn = 0; nn < 4; ++nn)
+        for (int m = 0; m < 4; ++m)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int r = m * 16 + 4 * (lane >> 4) + i, c = nn * 16 + lc;
-            *reinterpret_cast<float*>(st + slot_of(r, c >> 2) + (c & 3) * 4) = acc[m][4 * h + nn][i];
-          }
-      const int c0 = tn * kBN + wn * TM::kWTN + 64 * h;
+          for (int nn = 0; nn < 4; ++nn)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int q = lane + 64 * j, r = q >> 4, c4 = q & 15;
-        const int row = r0 + r;
-        if (row < M)
-          *reinterpret_cast<f32x4*>(P + size_t(row) * ep.np + c0 + 4 * c4) =
-              *reinterpret_cast<const f32x4*>(st + slot_of(r, c4));
+            for (int i = 0; i < 4; ++i) {
+              const int r = m * 16 + 4 * (lane >> 4) + i, c = nn * 16 + lc;
+              *reinterpret_cast<float*>(st + slot_of(r, c >> 2) + (c & 3) * 4) = acc[4 * g + m][4 * h + nn][i];
+            }
+        const int c0 = tn * kBN + wn * TM::kWTN + 64 * h;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int q = lane + 64 * j, r = q >> 4, c4 = q & 15;
+          const int row = r0 + r;
+          if (row < M)
+            *reinterpret_cast<f32x4*>(P + size_t(row) * ep.np + c0 + 4 * c4) =
+                *reinterpret_cast<const f32x4*>(st + slot_of(r, c4));
+        }
       }
     }
   } else if constexpr (EPI == EPI_RESID) {
@@ -130,35 +133,38 @@ __global__ __launch_bounds__(Cfg::kThreads, 2) void gemm_kernel(const T* __restr
     // both the MFMA-layout writes and the row reads are conflict-free; then
     // every lane reads 16 bytes of x per access, all loads first (clamped
     // into the matrix) and the guarded stores after them.
-    static_assert(TM::kWTM == 64 && TM::kWTN == 128, "resid epilogue tiling");
+    static_assert(TM::kWTM % 64 == 0 && TM::kWTN == 128, "resid epilogue tiling");
     uint8_t* st = smem + wave * (64 * 64 * 4);
     auto slot_of = [](int r, int c4) { return r * 256 + (((c4 ^ (r & 15))) << 4); };
-    const int r0 = m0 + wm * 64;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int g = 0; g < TM::kWTM / 64; ++g) {   // 64-row groups of the wave tile
+      const int r0 = m0 + wm * TM::kWTM + 64 * g;
 #pragma unroll
-      for (int m = 0; m < TM::kFM; ++m)
+      for (int h = 0; h < 2; ++h) {
 #pragma unroll
-        for (int nn = 0; nn < 4; ++nn)
+        for (int m = 0; m < 4; ++m)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int r = m * 16 + 4 * (lane >> 4) + i, c = nn * 16 + lc;
-            *reinterpret_cast<float*>(st + slot_of(r, c >> 2) + (c & 3) * 4) = acc[m][4 * h + nn][i];
-          }
-      const int c0 = tn * kBN + wn * TM::kWTN + 64 * h;
-      f32x4 xv[16];
+          for (int nn = 0; nn < 4; ++nn)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int q = lane + 64 * j, r = q >> 4, c4 = q & 15;
-        const int row = min(r0 + r, M - 1), col = min(c0 + 4 * c4, N - 4);
-        xv[j] = *reinterpret_cast<const f32x4*>(ep.x + size_t(row) * ep.ldx + col);
-      }
+            for (int i = 0; i < 4; ++i) {
+              const int r = m * 16 + 4 * (lane >> 4) + i, c = nn * 16 + lc;
+              *reinterpret_cast<float*>(st + slot_of(r, c >> 2) + (c & 3) * 4) = acc[4 * g + m][4 * h + nn][i];
+            }
+        const int c0 = tn * kBN + wn * TM::kWTN + 64 * h;
+        f32x4 xv[16];
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int q = lane + 64 * j, r = q >> 4, c4 = q & 15;
-        const int row = r0 + r, col = c0 + 4 * c4;
-        const f32x4 a = *reinterpret_cast<const f32x4*>(st + slot_of(r, c4));
-        if (row < M && col < N) *reinterpret_cast<f32x4*>(ep.x + size_t(row) * ep.ldx + col) = xv[j] + a;
+        for (int j = 0; j < 16; ++j) {
+          const int q = lane + 64 * j, r = q >> 4, c4 = q & 15;
+          const int row = min(r0 + r, M - 1), col = min(c0 + 4 * c4, N - 4);
+          xv[j] = *reinterpret_cast<const f32x4*>(ep.x + size_t(row) * ep.ldx + col);
+        }
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int q = lane + 64 * j, r = q >> 4, c4 = q & 15;
+          const int row = r0 + r, col = c0 + 4 * c4;
+          const f32x4 a = *reinterpret_cast<const f32x4*>(st + slot_of(r, c4));
+          if (row < M && col < N) *reinterpret_cast<f32x4*>(ep.x + size_t(row) * ep.ldx + col) = xv[j] + a;
+        }
       }
     }
   } else if constexpr (EPI == EPI_SWIGLU) {

@@ -19,8 +19,18 @@ __global__ __launch_bounds__(kRowThreads) void embed_kernel(const int32_t* __res
   for (int c = threadIdx.x; c < d; c += kRowThreads) dst[c] = load_f(src + c);
 }
 
-// One workgroup per output row; the sum of squares is reduced in fp32 over
-// 4 waves.
+// store 4 consecutive values as one 8-byte (bf16) or 16-byte (fp32) access
+__device__ __forceinline__ void store4(bf16_t* p, f32x4 v) {
+  const uint32_t lo = uint32_t(f2bf(v.x)) | (uint32_t(f2bf(v.y)) << 16);
+  const uint32_t hi = uint32_t(f2bf(v.z)) | (uint32_t(f2bf(v.w)) << 16);
+  *reinterpret_cast<u32x2*>(p) = u32x2{lo, hi};
+}
+__device__ __forceinline__ void store4(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
+
+constexpr int kNormChunks = 8;   // 16-byte chunks per thread held in registers: d <= 8192
+
+// One workgroup per output row; the row stays in registers between the sum
+// of squares (reduced in fp32 over 4 waves) and the scaled store.
 template <typename T>
 __global__ __launch_bounds__(kRowThreads) void rmsnorm_kernel(const float* __restrict__ x, int d, float eps,
                                                               const int32_t* __restrict__ pos, int n_pos, int seq,
@@ -29,10 +39,13 @@ __global__ __launch_bounds__(kRowThreads) void rmsnorm_kernel(const float* __res
   const int r = blockIdx.x;
   const int src_row = pos ? (r / n_pos) * seq + min(max(pos[r % n_pos], 0), seq - 1) : r;
   const float* xr = x + size_t(src_row) * d;
+  f32x4 v[kNormChunks];
   float ss = 0.f;
-  for (int c = threadIdx.x * 4; c < d; c += kRowThreads * 4) {
-    const float4 v = *reinterpret_cast<const float4*>(xr + c);
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+#pragma unroll
+  for (int j = 0; j < kNormChunks; ++j) {
+    const int c = (threadIdx.x + j * kRowThreads) * 4;
+    v[j] = c < d ? *reinterpret_cast<const f32x4*>(xr + c) : f32x4{0.f, 0.f, 0.f, 0.f};
+    ss += v[j].x * v[j].x + v[j].y * v[j].y + v[j].z * v[j].z + v[j].w * v[j].w;
   }
   ss = wave_sum(ss);
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
@@ -42,12 +55,10 @@ __global__ __launch_bounds__(kRowThreads) void rmsnorm_kernel(const float* __res
   for (int w = 0; w < kRowThreads / kWave; ++w) tot += part[w];
   const float inv = 1.0f / sqrtf(tot / float(d) + eps);
   T* o = out + size_t(r) * d;
-  for (int c = threadIdx.x * 4; c < d; c += kRowThreads * 4) {
-    const float4 v = *reinterpret_cast<const float4*>(xr + c);
-    store_f(o + c + 0, v.x * inv);
-    store_f(o + c + 1, v.y * inv);
-    store_f(o + c + 2, v.z * inv);
-    store_f(o + c + 3, v.w * inv);
+#pragma unroll
+  for (int j = 0; j < kNormChunks; ++j) {
+    const int c = (threadIdx.x + j * kRowThreads) * 4;
+    if (c < d) store4(o + c, v[j] * inv);
   }
 }
 
@@ -62,20 +73,26 @@ __global__ __launch_bounds__(kRowThreads) void resid_rmsnorm_kernel(const float*
   const int r = blockIdx.x;
   float* xr = x + size_t(r) * d;
   auto pr = [&](int p, int c) { return *reinterpret_cast<const f32x4*>(part + (size_t(p) * M + r) * np + c); };
+  f32x4 v[kNormChunks];
   float ss = 0.f;
-  for (int c = threadIdx.x * 4; c < d; c += kRowThreads * 4) {
-    f32x4 v = *reinterpret_cast<const f32x4*>(xr + c);
-    int p = 0;
-    for (; p + 4 <= splits; p += 4) {   // four loads in flight, added in order
-      const f32x4 a0 = pr(p, c), a1 = pr(p + 1, c), a2 = pr(p + 2, c), a3 = pr(p + 3, c);
-      v += a0;
-      v += a1;
-      v += a2;
-      v += a3;
+#pragma unroll
+  for (int j = 0; j < kNormChunks; ++j) {
+    const int c = (threadIdx.x + j * kRowThreads) * 4;
+    v[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (c < d) {
+      v[j] = *reinterpret_cast<const f32x4*>(xr + c);
+      int p = 0;
+      for (; p + 4 <= splits; p += 4) {   // four loads in flight, added in order
+        const f32x4 a0 = pr(p, c), a1 = pr(p + 1, c), a2 = pr(p + 2, c), a3 = pr(p + 3, c);
+        v[j] += a0;
+        v[j] += a1;
+        v[j] += a2;
+        v[j] += a3;
+      }
+      for (; p < splits; ++p) v[j] += pr(p, c);
+      *reinterpret_cast<f32x4*>(xr + c) = v[j];
     }
-    for (; p < splits; ++p) v += pr(p, c);
-    *reinterpret_cast<f32x4*>(xr + c) = v;
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    ss += v[j].x * v[j].x + v[j].y * v[j].y + v[j].z * v[j].z + v[j].w * v[j].w;
   }
   ss = wave_sum(ss);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
@@ -85,12 +102,10 @@ __global__ __launch_bounds__(kRowThreads) void resid_rmsnorm_kernel(const float*
   for (int w = 0; w < kRowThreads / kWave; ++w) tot += red[w];
   const float inv = 1.0f / sqrtf(tot / float(d) + eps);
   T* o = out + size_t(r) * d;
-  for (int c = threadIdx.x * 4; c < d; c += kRowThreads * 4) {
-    const f32x4 v = *reinterpret_cast<const f32x4*>(xr + c);   // this thread's own writes
-    store_f(o + c + 0, v.x * inv);
-    store_f(o + c + 1, v.y * inv);
-    store_f(o + c + 2, v.z * inv);
-    store_f(o + c + 3, v.w * inv);
+#pragma unroll
+  for (int j = 0; j < kNormChunks; ++j) {
+    const int c = (threadIdx.x + j * kRowThreads) * 4;
+    if (c < d) store4(o + c, v[j] * inv);
   }
 }
 
@@ -120,6 +135,7 @@ hipError_t embed(int dtype, const int32_t* tok, int rows, const void* emb, int d
 
 hipError_t rmsnorm(int dtype, const float* x, int d, float eps, int rows, const int32_t* pos, int n_pos, int seq,
                    void* out, hipStream_t s) {
+  if (d % 4 || d > kNormChunks * kRowThreads * 4) return hipErrorInvalidValue;
   if (dtype)
     hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(rows), dim3(kRowThreads), 0, s, x, d, eps, pos, n_pos, seq,
                        static_cast<bf16_t*>(out));
@@ -131,7 +147,7 @@ hipError_t rmsnorm(int dtype, const float* x, int d, float eps, int rows, const 
 
 hipError_t resid_rmsnorm(int dtype, const float* part, int splits, int np, int M, float* x, int d, float eps,
                          void* out, hipStream_t s) {
-  if (d % 4 || np % 4) return hipErrorInvalidValue;
+  if (d % 4 || np % 4 || d > kNormChunks * kRowThreads * 4) return hipErrorInvalidValue;
   if (dtype)
     hipLaunchKernelGGL(resid_rmsnorm_kernel<bf16_t>, dim3(M), dim3(kRowThreads), 0, s, part, splits, np, M, x, d, eps,
                        static_cast<bf16_t*>(out));

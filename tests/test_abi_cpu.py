@@ -70,15 +70,15 @@ def _weights(_abi, L=2, null_layer=None):
 
 
 @pytest.mark.parametrize("field,value,status", [
-    ("head_dim", 96, 2), ("d_model", 320, 2), ("d_ffn", 1000, 2), ("dtype", 7, 3), ("mask_id", 1024, 1),
-    ("n_layers", 0, 2), ("rms_eps", 0.0, 1),
+    ("head_dim", 96, 2), ("d_model", 320, 2), ("d_model", 8448, 2), ("d_ffn", 1000, 2), ("dtype", 7, 3),
+    ("mask_id", 1024, 1), ("n_layers", 0, 2), ("rms_eps", 0.0, 1),
 ])
 def test_model_create_rejects_bad_desc(abi, field, value, status):
     _abi, lib = abi
     w, keep = _weights(_abi)
     kw = {field: value}
     if field == "d_model":
-        kw["n_heads"] = 5
+        kw["n_heads"] = value // 64
     h = C.c_void_p()
     assert lib.dllm_model_create(C.byref(_desc(_abi, **kw)), C.byref(w), C.byref(h)) == status
     assert _err(lib)
