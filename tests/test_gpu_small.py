@@ -118,6 +118,68 @@ def test_forward_small_bf16_against_mirror(P, small_bf16):
     print(compare_stats(out.numpy(), ref, 2e-2, margin="auto", label="forward small bf16"))
 
 
+def test_forward_tiny_f32_many_sequences(P, tiny):
+    """64 sequences of 200 tokens: the attention's pipelined schedule (256-query
+    tiles, three-slot key ring, ragged last tile); three sequences against the oracle."""
+    shape, w_np, model = tiny
+    B_, S = 64, 200
+    toks = synth.tokens_np(31, "toks", B_ * S, shape.vocab - 1).reshape(B_, S)
+    toks[:, 120:] = shape.mask_id
+    lm_pos = np.array([0, 63, 64, 119, 120, 150, 199], dtype=np.int32)
+    out = model.forward(torch.from_numpy(toks).to(DEV), torch.from_numpy(lm_pos).to(DEV), scale=2.0)
+    torch.cuda.synchronize()
+    got = out.numpy()
+    for b in (0, 17, 63):
+        logits = om.forward_logits(toks[b:b + 1], w_np, shape, lm_pos, scale=2.0)
+        ref = softmax_stats(logits.reshape(-1, shape.vocab), 16)
+        sl = slice(b * len(lm_pos), (b + 1) * len(lm_pos))
+        print(compare_stats({k: v[sl] for k, v in got.items()}, ref, 1e-4, label=f"64 x 200 f32 seq {b}"))
+
+
+def test_cached_prefix_many_blocks_tiny(P, tiny):
+    """A 40-position cached prefix shared by 64 blocks of 200 (pipelined
+    attention with prefix tiles); two blocks against the oracle."""
+    from paper_2608_11742_amd._abi import KvCache
+    shape, w_np, model = tiny
+    Pn, Bk, nb = 40, 200, 64
+    prefix = synth.tokens_np(32, "prefix", Pn, shape.vocab - 1)
+    k, vt, cap = model.new_kv_cache(Pn)
+    kvc = KvCache(k.data_ptr(), vt.data_ptr(), 0, cap)
+    model.forward(torch.from_numpy(prefix).to(DEV)[None], torch.arange(1, dtype=torch.int32, device=DEV),
+                  kv_out=kvc)
+    blocks = synth.tokens_np(33, "blocks", nb * Bk, shape.vocab - 1).reshape(nb, Bk)
+    blocks[:, 100:] = shape.mask_id
+    lm = np.array([0, 99, 100, 160, 199], dtype=np.int32)
+    kvc.len = Pn
+    out = model.forward(torch.from_numpy(blocks).to(DEV), torch.from_numpy(lm).to(DEV), pos_offset=Pn,
+                        kv_prefix=kvc, scale=4.0)
+    torch.cuda.synchronize()
+    got = out.numpy()
+    kv = om.prefix_cache(prefix, w_np, shape)
+    for b in (0, 33):
+        h = om.hidden(blocks[b], w_np, shape, pos_offset=Pn, prefix_kv=kv)
+        ref = softmax_stats(om.lm_logits(h[lm], w_np, shape, scale=4.0), 16)
+        sl = slice(b * len(lm), (b + 1) * len(lm))
+        print(compare_stats({k: v[sl] for k, v in got.items()}, ref, 1e-4, label=f"cached 64 x 200 block {b}"))
+
+
+def test_forward_small_bf16_many_sequences(P, small_bf16):
+    shape, w_np, model = small_bf16
+    B_, S = 64, 200
+    toks = synth.tokens_np(34, "toks", B_ * S, shape.vocab - 1).reshape(B_, S)
+    toks[:, 100:] = shape.mask_id
+    lm_pos = np.arange(100, 200, 7, dtype=np.int32)
+    out = model.forward(torch.from_numpy(toks).to(DEV), torch.from_numpy(lm_pos).to(DEV), scale=3.0)
+    torch.cuda.synchronize()
+    got = out.numpy()
+    for b in (5, 62):
+        logits = om.forward_logits(toks[b:b + 1], w_np, shape, lm_pos, scale=3.0, mirror=True)
+        ref = softmax_stats(logits.reshape(-1, shape.vocab), 16)
+        sl = slice(b * len(lm_pos), (b + 1) * len(lm_pos))
+        print(compare_stats({k: v[sl] for k, v in got.items()}, ref, 2e-2, margin="auto",
+                            label=f"64 x 200 bf16 seq {b}"))
+
+
 @pytest.mark.parametrize("S", [40, 64])
 def test_forward_small_bf16_few_rows(P, small_bf16, S):
     """Few-row forwards (the 64-row GEMM tiles and split-K reductions of a
