@@ -28,7 +28,11 @@ struct GemmCfg {
 };
 using Big = GemmCfg<256, 256, 4, 2, 2>;
 using Small = GemmCfg<64, 256, 1, 2, 2>;
-constexpr int kBN = 256;          // both configurations
+// gate/up with 257-512 rows: 256 x 192 tiles (waves of 64 x 96, 48 gate + 48
+// up rows each) give 2 x F / 96 = 256 workgroups for the 8B shape, one per CU,
+// where 256 x 256 tiles leave a quarter of the CUs idle
+using Mid = GemmCfg<256, 192, 4, 2, 2>;
+constexpr int kBN = 256;          // Big and Small: column tile of the split-K partials and the QKV / residual launches
 constexpr int kGroupM = 8;
 #ifndef DLLM_SMALL_M_MAX
 #define DLLM_SMALL_M_MAX 64
@@ -76,12 +80,14 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
   auto b_off = [&](int r) -> uint32_t {
     int row;
     if constexpr (EPI == EPI_SWIGLU || EPI == EPI_PART_GU) {
-      // 256 B rows -> 128 outputs: each 128-row half of a wave column pairs 64 gate and 64 up rows
-      const int wn = r >> 7, rr = r & 127;
-      const int j = min(tn * 128 + wn * 64 + (rr & 63), ep.F - 1);
-      row = rr < 64 ? j : ep.F + j;
+      // BN rows -> BN / 2 outputs: each wave column of kWTN rows pairs kWTN / 2
+      // gate rows with the kWTN / 2 up rows of the same outputs
+      constexpr int kHalf = TM::kWTN / 2;
+      const int wn = r / TM::kWTN, rr = r % TM::kWTN;
+      const int j = min(tn * (Cfg::BN / 2) + wn * kHalf + rr % kHalf, ep.F - 1);
+      row = rr < kHalf ? j : ep.F + j;
     } else {
-      row = min(tn * kBN + r, N - 1);
+      row = min(tn * Cfg::BN + r, N - 1);
     }
     return uint32_t(row) * b_row_bytes + k_bytes;
   };
@@ -115,7 +121,7 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
               const int r = m * 16 + 4 * (lane >> 4) + i, c = nn * 16 + lc;
               *reinterpret_cast<float*>(st + slot_of(r, c >> 2) + (c & 3) * 4) = acc[4 * g + m][4 * h + nn][i];
             }
-        const int c0 = tn * kBN + wn * TM::kWTN + 64 * h;
+        const int c0 = tn * Cfg::BN + wn * TM::kWTN + 64 * h;
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
           const int q = lane + 64 * j, r = q >> 4, c4 = q & 15;
@@ -150,7 +156,7 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
               const int r = m * 16 + 4 * (lane >> 4) + i, c = nn * 16 + lc;
               *reinterpret_cast<float*>(st + slot_of(r, c >> 2) + (c & 3) * 4) = acc[4 * g + m][4 * h + nn][i];
             }
-        const int c0 = tn * kBN + wn * TM::kWTN + 64 * h;
+        const int c0 = tn * Cfg::BN + wn * TM::kWTN + 64 * h;
         f32x4 xv[16];
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
@@ -177,7 +183,7 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
         if (row >= M) continue;
 #pragma unroll
         for (int n = 0; n < TM::kFN / 2; ++n) {
-          const int j = tn * 128 + wn * 64 + n * 16 + lc;
+          const int j = tn * (Cfg::BN / 2) + wn * (TM::kWTN / 2) + n * 16 + lc;
           if (j >= ep.F) continue;
           const float g = acc[m][n][i], u = acc[m][n + TM::kFN / 2][i];
           const float silu = g / (1.0f + __expf(-g));
@@ -188,7 +194,7 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
     static_assert(HD == 64 || HD == 128, "head_dim");
     const QkvOut& o = ep.qkv;
     constexpr int hd = HD, half = HD / 2, pair = HD / 32;  // partner block distance
-    const int wcol0 = tn * kBN + wn * TM::kWTN;            // first column of this wave tile
+    const int wcol0 = tn * Cfg::BN + wn * TM::kWTN;        // first column of this wave tile
     const int which = wcol0 / o.d;                         // 0: q, 1: k, 2: v (uniform per wave)
     const int cin0 = wcol0 % o.d;
     // rotary embedding in registers: (x1, x2) = columns (dim, dim + hd/2) of one head
@@ -503,6 +509,11 @@ hipError_t gemm_swiglu(int dtype, const void* A, int lda, const void* Wgu, int M
   EpiParams ep{};
   ep.out = out;
   ep.F = F;
+  if (!(sk && sk->splits > 1) && M > 256 && M <= 512 && M > kSmallM) {
+    const int tm = cdiv(F, Mid::BN / 2);
+    return dtype ? launch_cfg<bf16_t, EPI_SWIGLU, 0, Mid>(A, lda, Wgu, K, M, 2 * F, K, tm, ep, s, 1)
+                 : launch_cfg<float, EPI_SWIGLU, 0, Mid>(A, lda, Wgu, K, M, 2 * F, K, tm, ep, s, 1);
+  }
   const int tn = cdiv(F, 128);
   if (sk && sk->splits > 1) {
     if (F % 4) return hipErrorInvalidValue;
