@@ -41,8 +41,8 @@ METRIC = "denoising steps/sec and committed tokens/sec, 8B-shape, lookahead batc
 # the same counter reads for a plain device copy of known size (the
 # --copy-calibration mode).  Valid only for the kernel sources they were
 # measured on: bench.py reports null once those files change.
-TRAFFIC_GATEUP = {"fetch_bytes": 2418001803, "write_bytes": 201345536,
-                  "sources_sha256": "75ad6405c6f21f11c84ef9c54a7f7d204f3f8be11dcf0e76c52217c79e4b32d6"}
+TRAFFIC_GATEUP = {"fetch_bytes": 2417256558, "write_bytes": 201353728,
+                  "sources_sha256": "70e20eec13d6682944662e3b2a61c70851221b25c32de87639c54b89c6a55b3b"}
 TRAFFIC_SOURCES = ("paper_2608_11742_amd/csrc/gemm.hip", "paper_2608_11742_amd/csrc/mainloop.h",
                    "paper_2608_11742_amd/csrc/common.h")
 
@@ -99,7 +99,7 @@ def step_flops(shape, batch, seq, lm_rows):
     return shape.n_layers * per_layer + 2.0 * lm_rows * shape.d_model * shape.vocab
 
 
-def cpu_baseline(wl, w_dev, tokens_np, m_pos_np, n_layers_sample=2, lm_rows_sample=64):
+def cpu_baseline(wl, w_dev, tokens_np, m_pos_np, n_layers_sample=16, lm_rows_sample=256):
     """Oracle (float64 numpy, bf16 rounding at the GPU's storage points) on a bounded sample."""
     from threadpoolctl import threadpool_info
     from oracle import model as om
