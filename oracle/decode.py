@@ -51,10 +51,12 @@ def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps
     branch differs from the anchor inside the current block only).
     block_forward: optional ``block_forward(tokens, block_start)``, called at
     every block opening, that returns the model used for every later forward
-    of that block (e.g. a prefix-cached model built from the opening state)."""
+    of that block (e.g. a prefix-cached model built from the opening state),
+    or a pair (that model, a lookahead model as ``lookahead`` above) when the
+    lookahead of the block has a model of its own (packed over the cache)."""
     import dataclasses
     if lookahead is not None and block_forward is not None:
-        raise ValueError("a packed lookahead over a prefix cache is not modelled")
+        raise ValueError("pass the lookahead of a block model through block_forward")
     prm = dataclasses.replace(prm, max_branch=min(prm.max_branch, capacity - 1))   # slot 0: anchor
     prompt = np.asarray(prompt, dtype=np.int64)
     P = len(prompt)
@@ -67,7 +69,8 @@ def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps
         stats = forward(tokens[None, :], m_pos, None)[0][0]
         res.nfe += 1
         res.normal += 1
-        fwd_b = forward if block_forward is None else block_forward(tokens.copy(), P + b * block)
+        fb = None if block_forward is None else block_forward(tokens.copy(), P + b * block)
+        fwd_b, look_b = fb if isinstance(fb, tuple) else (fb or forward, lookahead)
         state = rps.State(tokens, m_pos, stats)
         while len(state.m_pos) > 0:
             iters += 1
@@ -89,10 +92,10 @@ def rps_decode(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps
             pv = plan.pivots[0]
             batch = rps.branch_tokens(state.tokens, plan, with_anchor=True)
             probe = [(pv.row, t) for t in pv.tokens]
-            if lookahead is None:
+            if look_b is None:
                 outs = fwd_b(batch, state.m_pos, probe)
             else:
-                outs = lookahead(batch, state.m_pos, probe, P + b * block, block)
+                outs = look_b(batch, state.m_pos, probe, P + b * block, block)
             res.nfe += 1
             res.lookahead += 1
             anchor, anchor_probe = outs[0]
@@ -136,7 +139,8 @@ def baseline_decode(forward, prompt, gen_len: int, block: int, mask_id: int, rul
             assert iters <= max_iters
             stats = (forward if fwd_b is None else fwd_b)(tokens[None, :], m_pos, None)[0][0]
             if fwd_b is None:
-                fwd_b = forward if block_forward is None else block_forward(tokens.copy(), P + b * block)
+                fb = forward if block_forward is None else block_forward(tokens.copy(), P + b * block)
+                fwd_b = fb[0] if isinstance(fb, tuple) else fb
             res.nfe += 1
             res.normal += 1
             state = rps.State(tokens, m_pos, stats)
@@ -201,7 +205,7 @@ def model_packed_lookahead(weights, shape, topk: int = 16, scales=None, scale: f
 
 
 def model_prefix_cached(weights, shape, topk: int = 16, scales=None, scale: float = 1.0,
-                        mirror: bool = False):
+                        mirror: bool = False, packed: bool = False):
     """Block-forward factory for ``rps_decode`` and ``baseline_decode``: the
     prefix cache the paper combines RPS with (Fast-dLLM's; Section 5.3, KV caching).
 
@@ -211,9 +215,16 @@ def model_prefix_cached(weights, shape, topk: int = 16, scales=None, scale: floa
     from the block start to the end of the sequence (the block and the masked
     suffix), attending to those cached keys and values plus its own.  Cached
     rows do not see commits made after the block opened (the approximation).
+    packed: the factory returns (forward, lookahead), the lookahead being the
+    packed sequence [block + suffix || branch blocks] over the same cache.
     """
-    from .model import hidden, lm_logits
+    from .model import hidden, lm_logits, packed_logits
     from .stats import softmax_stats
+
+    def stats_of(logits, probe):
+        st = softmax_stats(logits, topk)
+        pl = None if probe is None else [float(logits[row, tok] - st.lse[row]) for row, tok in probe]
+        return st, pl
 
     def open_block(tokens, block_start):
         kv = []
@@ -228,10 +239,20 @@ def model_prefix_cached(weights, shape, topk: int = 16, scales=None, scale: floa
             out = []
             for toks in np.asarray(batch):
                 h = hidden(toks[block_start:], weights, shape, pos_offset=block_start, mirror=mirror, prefix_kv=ctx)
-                logits = lm_logits(h[rel], weights, shape, row_scale=rs, scale=scale)
-                st = softmax_stats(logits, topk)
-                pl = None if probe is None else [float(logits[row, tok] - st.lse[row]) for row, tok in probe]
-                out.append((st, pl))
+                out.append(stats_of(lm_logits(h[rel], weights, shape, row_scale=rs, scale=scale), probe))
             return out
-        return fwd
+
+        def look(batch, m_pos, probe, b0, B):
+            assert b0 == block_start
+            batch = np.asarray(batch)
+            tail = batch[0, b0:]
+            assert np.all(batch[1:, b0 + B:] == tail[B:]), "branches differ from the anchor outside the block"
+            tokens = np.concatenate([tail] + [row[b0:b0 + B] for row in batch[1:]])
+            m_pos = np.asarray(m_pos)
+            rs = None if scales is None else np.asarray(scales)[m_pos]
+            logits = packed_logits(tokens, weights, shape, len(tail), 0, B, batch.shape[0] - 1, m_pos - b0,
+                                   pos_offset=b0, mirror=mirror, row_scale=rs, scale=scale, prefix_kv=ctx)
+            return [stats_of(logits[c], probe) for c in range(logits.shape[0])]
+
+        return (fwd, look) if packed else fwd
     return open_block

@@ -83,7 +83,8 @@ def layer(x, weights, l, shape, pos, mirror=False, prefix_kv=None, collect=None,
     (k, v) of a cached prefix, each [H, P, hd] (post-RoPE); the S block
     positions then attend to the prefix keys followed by their own keys.
     collect: optional list that receives this layer's (k, v), each [H, S, hd].
-    mask: optional boolean [S, S] attention mask (no prefix).
+    mask: optional boolean attention mask over the keys, [S, S], or
+    [S, P + S] with a prefix.
     """
     R = bf16_round if mirror else (lambda t: t)
     S, d = x.shape
@@ -188,27 +189,34 @@ def packed_layout(shared_len: int, block_start: int, block_len: int, n_branch: i
 
 
 def packed_hidden(tokens, weights, shape, shared_len, block_start, block_len, n_branch, pos_offset=0,
-                  mirror=False):
+                  mirror=False, prefix_kv=None):
     """Final normed hidden states of every row of a packed lookahead sequence
-    (tokens [S + n*B]); layout and mask of ``packed_layout``."""
+    (tokens [S + n*B]); layout and mask of ``packed_layout``.  prefix_kv:
+    optional per-layer cached (k, v) of positions before pos_offset, visible
+    to every row (the prefix cache; the packed rows then start at pos_offset)."""
     tokens = np.asarray(tokens, dtype=np.int64)
     pos, mask = packed_layout(shared_len, block_start, block_len, n_branch, pos_offset)
     assert tokens.shape[0] == pos.shape[0]
     x = _w(weights, "emb")[tokens]
     for l in range(shape.n_layers):
-        x = layer(x, weights, l, shape, pos, mirror=mirror, mask=mask)
+        if prefix_kv is None:
+            x = layer(x, weights, l, shape, pos, mirror=mirror, mask=mask)
+        else:
+            P = prefix_kv[l][0].shape[1]
+            full = np.concatenate([np.ones((mask.shape[0], P), dtype=bool), mask], axis=1)
+            x = layer(x, weights, l, shape, pos, mirror=mirror, prefix_kv=prefix_kv[l], mask=full)
     h = rmsnorm(x, shape.rms_eps)
     return bf16_round(h) if mirror else h
 
 
 def packed_logits(tokens, weights, shape, shared_len, block_start, block_len, n_branch, lm_pos, pos_offset=0,
-                  mirror=False, row_scale=None, scale=1.0):
+                  mirror=False, row_scale=None, scale=1.0, prefix_kv=None):
     """Logits of a packed lookahead forward at positions lm_pos of the shared
     sequence, for the anchor and then for every branch: [1 + n, len(lm_pos), V].
     A branch reads its own row where the position lies in the block, else the
     shared row.  row_scale: optional per-position scale indexed like lm_pos."""
     S, b0, B = shared_len, block_start, block_len
-    h = packed_hidden(tokens, weights, shape, S, b0, B, n_branch, pos_offset, mirror)
+    h = packed_hidden(tokens, weights, shape, S, b0, B, n_branch, pos_offset, mirror, prefix_kv=prefix_kv)
     lm_pos = np.asarray(lm_pos, dtype=np.int64)
     out = []
     for c in range(-1, n_branch):

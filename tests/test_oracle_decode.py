@@ -186,3 +186,34 @@ def test_prefix_cached_decode_invariants():
                      block_forward=model_prefix_cached(w, shape, scales=scales))
     _check_trace(res, P, G, B, shape.mask_id)
     assert res.nfe == res.normal + res.lookahead and res.nfe <= G
+
+
+def test_packed_lookahead_over_the_cache_with_one_layer_is_exact():
+    # one layer: the cache and the packing are both exact, so the packed cached
+    # decode takes the plain decode's path
+    shape = synth.ModelShape(n_layers=1, d_model=64, n_heads=4, head_dim=16, d_ffn=96, vocab=101)
+    w = synth.model_weights_np(shape, seed=4, dtype="f32")
+    P, G, B = 8, 32, 16
+    prompt = synth.tokens_np(3, "prompt", P, shape.vocab - 1)
+    scales = synth.position_scales_np(4, np.arange(P + G), 2.6, 16.0)
+    prm = rps.Params(mode="paper", k_max=8, tau_pivot=0.5, r=0.05, n_cand=8)
+    fwd = model_forward(w, shape, scales=scales)
+    a = rps_decode(fwd, prompt, G, B, shape.mask_id, prm, lam=0.1, tau=0.9)
+    b = rps_decode(fwd, prompt, G, B, shape.mask_id, prm, lam=0.1, tau=0.9,
+                   block_forward=model_prefix_cached(w, shape, scales=scales, packed=True))
+    assert a.lookahead > 0
+    assert np.array_equal(a.tokens, b.tokens)
+    assert [t[:-1] for t in a.trace] == [t[:-1] for t in b.trace]
+
+
+def test_packed_lookahead_over_the_cache_decode_invariants():
+    shape = synth.TINY
+    w = synth.model_weights_np(shape, seed=0, dtype="f32")
+    P, G, B = 16, 64, 32
+    prompt = synth.tokens_np(1, "prompt", P, shape.vocab - 1)
+    scales = synth.position_scales_np(2, np.arange(P + G), 2.6, 16.0)
+    prm = rps.Params(mode="paper", k_max=10, tau_pivot=0.9, r=0.1, n_cand=10)
+    res = rps_decode(model_forward(w, shape, scales=scales), prompt, G, B, shape.mask_id, prm, lam=0.1, tau=0.9,
+                     block_forward=model_prefix_cached(w, shape, scales=scales, packed=True))
+    _check_trace(res, P, G, B, shape.mask_id)
+    assert res.nfe == res.normal + res.lookahead and res.nfe <= G

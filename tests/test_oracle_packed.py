@@ -150,3 +150,36 @@ def test_packed_logits_rows():
         assert np.allclose(lg[1 + c][[0, 4]], anchor[[0, 4]], atol=1e-10)    # outside the block: shared rows
         ref = om.lm_logits(h[14 + 4 * c + np.array([0, 1, 3])], w, TWO, row_scale=rs[[6, 7, 9]], scale=1.3)
         assert np.allclose(lg[1 + c][1:4], ref, atol=1e-10)
+
+
+def _prefix(shape, w, n=9, seed=11):
+    toks = np.random.default_rng(seed).integers(0, shape.vocab - 1, n)
+    kv = []
+    om.hidden(toks, w, shape, collect=kv)
+    return toks, kv
+
+
+def test_packed_over_a_prefix_without_branches_is_the_cached_forward():
+    w = _weights(TWO, seed=7)
+    _, kv = _prefix(TWO, w)
+    shared, _, _ = _case(TWO, seed=7)
+    h = om.packed_hidden(shared, w, TWO, 14, 0, 4, 0, pos_offset=9, prefix_kv=kv)
+    ref = om.hidden(shared, w, TWO, pos_offset=9, prefix_kv=kv)
+    assert np.allclose(h, ref, atol=1e-12)
+
+
+def test_packed_over_a_prefix_matches_the_cached_forwards():
+    # shared rows: the cached forward of the shared sequence; branch rows: the
+    # block alone over the prefix plus the anchor's keys outside the block
+    w = _weights(TWO, seed=8)
+    _, kv = _prefix(TWO, w)
+    shared, branches, packed = _case(TWO, S=14, b0=0, B=4, seed=8)
+    h = om.packed_hidden(packed, w, TWO, 14, 0, 4, 3, pos_offset=9, prefix_kv=kv)
+    anchor = []
+    ref = om.hidden(shared, w, TWO, pos_offset=9, prefix_kv=kv, collect=anchor)
+    assert np.allclose(h[:14], ref, atol=1e-12)
+    ctx = [(np.concatenate([pk, ak[:, 4:]], axis=1), np.concatenate([pv, av[:, 4:]], axis=1))
+           for (pk, pv), (ak, av) in zip(kv, anchor)]
+    for c, blk in enumerate(branches):
+        hb = om.hidden(blk, w, TWO, pos_offset=9, prefix_kv=ctx)
+        assert np.allclose(h[14 + 4 * c:18 + 4 * c], hb, atol=1e-12)
