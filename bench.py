@@ -215,7 +215,7 @@ def other_configs(P, model, shape, n):
     log(f"{wl.name}: {wall:.2f} s, NFE {st.nfe}")
 
     # the same decode with the lookahead packed into one sequence (branch-isolating
-    # mask), and with the prefix cache refreshed at every block opening
+    # mask), with the prefix cache refreshed at every block opening, and both
     rps_row = out[wl.name]
 
     def variant(**kw):
@@ -234,6 +234,8 @@ def other_configs(P, model, shape, n):
     log(f"{wl.name} packed: {wall_p:.2f} s, NFE {sp.nfe}")
     sc, wall_c, rps_row["prefix_cache"] = variant(prefix_cache=True)
     log(f"{wl.name} prefix cache: {wall_c:.2f} s, NFE {sc.nfe}")
+    spc, wall_pc, rps_row["packed_prefix_cache"] = variant(packed=True, prefix_cache=True)
+    log(f"{wl.name} packed lookahead + prefix cache: {wall_pc:.2f} s, NFE {spc.nfe}")
 
     # the baselines of Section 3 on the same model, prompt and scales: Default
     # (one most confident token per forward) and Confidence (threshold 0.9),
@@ -251,7 +253,8 @@ def other_configs(P, model, shape, n):
                                        "wall_s": round(wall_b, 3), "nfe": sb.nfe}
         rps_row[f"speedup_vs_{name}"] = {"nfe": round(sb.nfe / st.nfe, 2), "tps": round(wall_b / wall, 2),
                                          "tps_packed": round(wall_b / wall_p, 2),
-                                         "tps_prefix_cache": round(wall_b / wall_c, 2)}
+                                         "tps_prefix_cache": round(wall_b / wall_c, 2),
+                                         "tps_packed_prefix_cache": round(wall_b / wall_pc, 2)}
         log(f"{wl.name} baseline {name}: {wall_b:.2f} s, NFE {sb.nfe}")
     return out
 

@@ -188,7 +188,12 @@ dllm_status dllm_forward(dllm_model* m, const int32_t* tokens, int32_t batch, in
  *                these rows.
  *   row_scale    nullable [shared_len] float indexed by in-sequence position
  *                (a branch row uses the scale of the position it copies).
- *   Other arguments as dllm_forward (batch 1, no KV cache).  The workspace is
+ *   kv_prefix    nullable cached prefix (Section 5.3's prefix cache) that every
+ *                row of the packed sequence attends to in full; the packed
+ *                rows then start at position pos_offset (typically the block:
+ *                shared sequence = the block and the masked suffix, with
+ *                block_start 0).
+ *   Other arguments as dllm_forward (batch 1, no kv_out).  The workspace is
  *   dllm_workspace_bytes_packed(m, shared_len, block_len, n_branch, n_lm_pos).
  * Errors: DLLM_ESHAPE unless 1 <= n_lm_pos <= shared_len, block_len is a
  *   power of two, n_branch >= 0, 0 <= block_start, block_start + block_len <=
@@ -196,9 +201,10 @@ dllm_status dllm_forward(dllm_model* m, const int32_t* tokens, int32_t batch, in
 size_t dllm_workspace_bytes_packed(const dllm_model* m, int32_t shared_len, int32_t block_len, int32_t n_branch,
                                    int32_t n_lm_pos);
 dllm_status dllm_forward_packed(dllm_model* m, const int32_t* tokens, int32_t shared_len, int32_t block_start,
-                                int32_t block_len, int32_t n_branch, int32_t pos_offset, const int32_t* lm_pos,
-                                int32_t n_lm_pos, const float* row_scale, float scale, const dllm_probe* probe,
-                                const dllm_stats* out, void* ws, size_t ws_bytes, dllm_stream stream);
+                                int32_t block_len, int32_t n_branch, int32_t pos_offset, const dllm_kv_cache* kv_prefix,
+                                const int32_t* lm_pos, int32_t n_lm_pos, const float* row_scale, float scale,
+                                const dllm_probe* probe, const dllm_stats* out, void* ws, size_t ws_bytes,
+                                dllm_stream stream);
 
 /* LM head with fused vocabulary statistics (the per-position quantities of
  * Section 3, Notation, that Eq. 1-4 consume): for each of R rows of final

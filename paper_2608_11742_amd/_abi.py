@@ -81,8 +81,8 @@ SIGNATURES = {
     "dllm_workspace_bytes_packed": (sz, [vp, i32, i32, i32, i32]),
     "dllm_forward": (i32, [vp, vp, i32, i32, i32, C.POINTER(KvCache), C.POINTER(KvCache), vp, i32, vp, f32,
                            C.POINTER(Probe), C.POINTER(StatsC), vp, sz, vp]),
-    "dllm_forward_packed": (i32, [vp, vp, i32, i32, i32, i32, i32, vp, i32, vp, f32, C.POINTER(Probe),
-                                  C.POINTER(StatsC), vp, sz, vp]),
+    "dllm_forward_packed": (i32, [vp, vp, i32, i32, i32, i32, i32, C.POINTER(KvCache), vp, i32, vp, f32,
+                                  C.POINTER(Probe), C.POINTER(StatsC), vp, sz, vp]),
     "vocab_entropy_topk_workspace_bytes": (sz, [i32, i32]),
     "vocab_entropy_topk": (i32, [vp, vp, i32, i32, i32, i32, vp, f32, i32, C.POINTER(StatsC), vp, sz, vp]),
     "dllm_profile_begin": (i32, [vp, i32]),

@@ -167,15 +167,15 @@ def dllm_forward(handle, tokens, lm_pos, out: Stats, ws, pos_offset: int = 0, ro
 
 
 def dllm_forward_packed(handle, tokens, shared_len: int, block_start: int, block_len: int, n_branch: int, lm_pos,
-                        out: Stats, ws, pos_offset: int = 0, row_scale=None, scale: float = 1.0,
-                        probe: Probe | None = None, n_lm_pos: int | None = None, stream=None):
+                        out: Stats, ws, pos_offset: int = 0, kv_prefix: KvCache | None = None, row_scale=None,
+                        scale: float = 1.0, probe: Probe | None = None, n_lm_pos: int | None = None, stream=None):
     """Packed lookahead forward: tokens [shared_len + n_branch * block_len] (one
     sequence); out receives (1 + n_branch) * n_lm_pos rows (shared, then each branch)."""
     n_lm = lm_pos.shape[0] if n_lm_pos is None else n_lm_pos
     _check(lib().dllm_forward_packed(handle, _p(tokens), shared_len, block_start, block_len, n_branch, pos_offset,
-                                     _p(lm_pos), n_lm, _p(row_scale), scale,
-                                     None if probe is None else C.byref(probe), C.byref(out.c()), _p(ws),
-                                     ws.numel() * ws.element_size(), _stream(stream)))
+                                     None if kv_prefix is None else C.byref(kv_prefix), _p(lm_pos), n_lm,
+                                     _p(row_scale), scale, None if probe is None else C.byref(probe),
+                                     C.byref(out.c()), _p(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def vocab_entropy_topk_workspace_bytes(R: int, vocab: int) -> int:

@@ -284,7 +284,7 @@ dllm_status forward_impl(dllm_model* m, const int32_t* tokens, int32_t batch, in
   if (pos_offset < 0 || pos_offset + n_pos > d.max_pos)
     return fail(DLLM_ESHAPE, "positions %d..%d exceed max_pos %d", pos_offset, pos_offset + n_pos - 1, d.max_pos);
   if (pk) {
-    if (batch != 1 || kv_prefix || kv_out) return fail(DLLM_EINVAL, "packed lookahead: batch 1, no KV cache");
+    if (batch != 1 || kv_out) return fail(DLLM_EINVAL, "packed lookahead: batch 1, no kv_out");
     if (pk->S < 1 || pk->B < 1 || (pk->B & (pk->B - 1)) || pk->n_branch < 0 || seq != pk->S + pk->n_branch * pk->B ||
         pk->b0 < 0 || pk->b0 + pk->B > pk->S)
       return fail(DLLM_ESHAPE, "packed lookahead: shared %d block %d..%d, seq %d", pk->S, pk->b0, pk->b0 + pk->B - 1,
@@ -458,13 +458,14 @@ dllm_status dllm_forward(dllm_model* m, const int32_t* tokens, int32_t batch, in
 }
 
 dllm_status dllm_forward_packed(dllm_model* m, const int32_t* tokens, int32_t shared_len, int32_t block_start,
-                                int32_t block_len, int32_t n_branch, int32_t pos_offset, const int32_t* lm_pos,
-                                int32_t n_lm_pos, const float* row_scale, float scale, const dllm_probe* probe,
-                                const dllm_stats* out, void* ws, size_t ws_bytes, dllm_stream stream) {
+                                int32_t block_len, int32_t n_branch, int32_t pos_offset, const dllm_kv_cache* kv_prefix,
+                                const int32_t* lm_pos, int32_t n_lm_pos, const float* row_scale, float scale,
+                                const dllm_probe* probe, const dllm_stats* out, void* ws, size_t ws_bytes,
+                                dllm_stream stream) {
   if (n_branch < 0 || block_len < 1 || shared_len < 1)
     return fail(DLLM_ESHAPE, "packed lookahead: shared %d, %d branches of %d", shared_len, n_branch, block_len);
   const Packing pk{shared_len, block_start, block_len, n_branch};
-  return forward_impl(m, tokens, 1, shared_len + n_branch * block_len, pos_offset, nullptr, nullptr, lm_pos,
+  return forward_impl(m, tokens, 1, shared_len + n_branch * block_len, pos_offset, kv_prefix, nullptr, lm_pos,
                       n_lm_pos, row_scale, scale, probe, out, ws, ws_bytes, stream, &pk);
 }
 

@@ -115,12 +115,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
     const uint8_t* v;
     int k0, nk, ld;
     int branch;   // phase-2 tile: the branch block it covers; -1 otherwise
+    bool prefix;  // a tile of the cached prefix (visible to every query)
   };
   auto src = [&](int t) -> Src {
-    if (t < n_pt) return Src{Kp, Vp, t * kKT, a.p_len, a.p_cap, -1};
-    if (t < n_pt + n_ot) return Src{Ko, Vo, (t - n_pt) * kKT, S, a.vt_ld, -1};
+    if (t < n_pt) return Src{Kp, Vp, t * kKT, a.p_len, a.p_cap, -1, true};
+    if (t < n_pt + n_ot) return Src{Ko, Vo, (t - n_pt) * kKT, S, a.vt_ld, -1, false};
     const int u = t - n_pt - n_ot, j = jb0 + u / tpb;
-    return Src{Ko, Vo, S + j * a.pack_B + (u % tpb) * kKT, S + (j + 1) * a.pack_B, a.vt_ld, j};
+    return Src{Ko, Vo, S + j * a.pack_B + (u % tpb) * kKT, S + (j + 1) * a.pack_B, a.vt_ld, j, false};
   };
   // Copy tile t into ring slot `slot`.  Lane l of a load instruction fills
   // row l / C, slot l % C of its block and fetches the chunk the swizzle
@@ -189,8 +190,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
     const Src sr = src(t);
     const int k0 = sr.k0, nk = sr.nk;
     // does the packing mask keys of this tile?  phase 2 always; phase 1 where
-    // the tile meets the stood-in block and the workgroup has branch queries
-    const bool pmask = packed && (sr.branch >= 0 || (n_bt > 0 && k0 < a.pack_b0 + a.pack_B && k0 + kKT > a.pack_b0));
+    // the tile meets the stood-in block and the workgroup has branch queries;
+    // never a tile of the cached prefix
+    const bool pmask = packed && !sr.prefix &&
+                       (sr.branch >= 0 || (n_bt > 0 && k0 < a.pack_b0 + a.pack_B && k0 + kKT > a.pack_b0));
 
     // the tile's 64 keys in two halves of 32: S^T, online softmax and P V per half
 #pragma unroll
@@ -332,7 +335,7 @@ template <typename T, int HD>
 hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
   // the V^T copies read whole 16-byte chunks inside each row of pitch vt_ld / p_cap
   if (a.vt_ld < 8 || a.vt_ld % 8 || (a.kp && (a.p_cap < 8 || a.p_cap % 8))) return hipErrorInvalidValue;
-  if (a.pack_B > 0 && (a.B != 1 || a.kp || a.pack_S < 1 || a.pack_S > a.Sq || (a.Sq - a.pack_S) % a.pack_B ||
+  if (a.pack_B > 0 && (a.B != 1 || a.pack_S < 1 || a.pack_S > a.Sq || (a.Sq - a.pack_S) % a.pack_B ||
                        a.pack_b0 < 0 || a.pack_b0 + a.pack_B > a.pack_S))
     return hipErrorInvalidValue;
   const float scale = 1.4426950408889634f / sqrtf(float(HD));

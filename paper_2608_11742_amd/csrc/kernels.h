@@ -67,9 +67,10 @@ struct AttnArgs {
   const void* vpt;   // prefix values^T [H][hd][cap]
   int p_len, p_cap;
   void* o;           // [B*Sq][H*hd]
-  // packed lookahead (B == 1, no prefix): rows 0 .. pack_S-1 are the shared
-  // sequence, then branch blocks of pack_B rows, each standing in for rows
-  // pack_b0 .. pack_b0+pack_B-1; pack_B == 0: no packing
+  // packed lookahead (B == 1): rows 0 .. pack_S-1 are the shared sequence,
+  // then branch blocks of pack_B rows, each standing in for rows
+  // pack_b0 .. pack_b0+pack_B-1; a cached prefix stays visible to every row;
+  // pack_B == 0: no packing
   int pack_S = 0, pack_b0 = 0, pack_B = 0;
 };
 hipError_t attention(int dtype, const AttnArgs& a, hipStream_t s);

@@ -81,7 +81,8 @@ class Model:
 
     def forward_packed(self, tokens, shared_len: int, block_start: int, block_len: int, n_branch: int, lm_pos,
                        out: B.Stats | None = None, n_lm_pos: int | None = None, row_scale=None, scale: float = 1.0,
-                       pos_offset: int = 0, probe=None, k: int = 16, stream=None) -> B.Stats:
+                       pos_offset: int = 0, kv_prefix: KvCache | None = None, probe=None, k: int = 16,
+                       stream=None) -> B.Stats:
         """Packed lookahead forward over [shared || n_branch block copies] (one
         sequence, branch-isolating mask); returns (1 + n_branch) * n_lm_pos rows."""
         n = lm_pos.shape[0] if n_lm_pos is None else n_lm_pos
@@ -89,6 +90,6 @@ class Model:
             out = B.Stats((1 + n_branch) * n, k, device=self.device)
         ws = self.workspace_packed(shared_len, block_len, n_branch, n)
         B.dllm_forward_packed(self.handle, tokens, shared_len, block_start, block_len, n_branch, lm_pos, out, ws,
-                              pos_offset=pos_offset, row_scale=row_scale, scale=scale, probe=probe, n_lm_pos=n,
-                              stream=stream)
+                              pos_offset=pos_offset, kv_prefix=kv_prefix, row_scale=row_scale, scale=scale,
+                              probe=probe, n_lm_pos=n, stream=stream)
         return out

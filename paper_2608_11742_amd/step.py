@@ -120,6 +120,17 @@ class _BlockView:
     def offset(self) -> int:
         return 0 if self.kv is None else self.b0
 
+    def forward_packed(self, tok, block: int, nb: int, m_pos, out, n: int, probe=None):
+        """Packed lookahead [seq || nb copies of the block] (tok: the packed tokens)."""
+        L = self.seq.shape[0]
+        if self.kv is None:
+            self.model.forward_packed(tok, L, self.b0, block, nb, m_pos, out=out, n_lm_pos=n,
+                                      row_scale=self.row_scale, scale=self.scale, probe=probe)
+            return
+        rs = None if self.row_scale is None else self.row_scale[self.b0:]
+        self.model.forward_packed(tok, L, 0, block, nb, m_pos, out=out, n_lm_pos=n, row_scale=rs, scale=self.scale,
+                                  pos_offset=self.b0, kv_prefix=self.kv if self.b0 > 0 else None, probe=probe)
+
     def forward(self, tok, m_pos, out, n: int, probe=None):
         if self.kv is None:
             self.model.forward(tok, m_pos, out=out, n_lm_pos=n, row_scale=self.row_scale, scale=self.scale,
@@ -144,12 +155,11 @@ def rps_decode(model, prompt, gen_len: int, block: int, prm, lam: float, tau: fl
     1 + n full sequences; block must then be a power of two.
     prefix_cache: refresh a prefix KV cache at every block opening and run the
     block's later forwards (normal and lookahead) on the block and the masked
-    suffix only (see _BlockView).
+    suffix only (see _BlockView); with packed, the packed sequence is [block +
+    suffix || block copies] over the cached prefix.
     """
     if prm.max_branch > capacity - 1:
         raise ValueError("prm.max_branch must leave slot 0 of the lookahead batch to the anchor")
-    if packed and prefix_cache:
-        raise ValueError("packed lookahead over a prefix cache is not supported")
     dev = prompt.device
     P = prompt.shape[0]
     S = P + gen_len
@@ -218,10 +228,9 @@ def rps_decode(model, prompt, gen_len: int, block: int, prm, lam: float, tau: fl
             probe = Probe(B.plan_field_ptr(plan, "br_row"), B.plan_field_ptr(plan, "br_token"),
                           anchor_logit.data_ptr(), nb)
             if packed:
-                B.rps_build_packed(tokens, plan, b0, block, nb, pk)
-                timed("lookahead", lambda: model.forward_packed(pk[:S + nb * block], S, b0, block, nb, m_pos,
-                                                                out=branch, n_lm_pos=n_m, row_scale=row_scale,
-                                                                scale=scale, probe=probe))
+                B.rps_build_packed(seq, plan, b0 - off, block, nb, pk)
+                timed("lookahead", lambda: view.forward_packed(pk[:L + nb * block], block, nb, m_pos, branch, n_m,
+                                                               probe=probe))
             else:
                 B.rps_build_branches(seq, plan, True, 1 + nb, bt)
                 timed("lookahead", lambda: view.forward(bt[:1 + nb], m_pos, branch, n_m, probe=probe))

@@ -151,7 +151,7 @@ def test_scheduler_validation(abi):
     assert lib.rps_build_packed(fake, 64, fake, 0, 8, _abi.RPS_MAX_BRANCH + 1, fake, None) == 2
     assert lib.rps_build_packed(fake, 64, None, 0, 8, 4, fake, None) == 1
     # packed forward without a model
-    assert lib.dllm_forward_packed(None, fake, 64, 0, 8, 2, 0, fake, 4, None, 1.0, None, C.byref(st), fake, 1 << 20,
+    assert lib.dllm_forward_packed(None, fake, 64, 0, 8, 2, 0, None, fake, 4, None, 1.0, None, C.byref(st), fake, 1 << 20,
                                    None) == 1
     assert lib.dllm_workspace_bytes_packed(None, 64, 8, 2, 4) == 0
 

@@ -183,3 +183,58 @@ def test_packed_decode_trajectory_matches_oracle(P, tiny, tau_pivot, lam, seed):
     assert st.lookahead > 0
     print(f"packed: nfe {st.nfe} (lookahead {st.lookahead}), pivot commits {st.commits_pivot}, "
           f"abstains {st.abstains}, first excluded event {excluded}")
+
+
+@pytest.mark.parametrize("Pn,S,B,n", [(40, 96, 32, 4), (77, 64, 64, 3), (130, 32, 32, 10)])
+def test_packed_forward_over_a_prefix_tiny_f32(P, tiny, Pn, S, B, n):
+    """The packed lookahead of a cached block: [block + suffix || block copies]
+    (block_start 0) attending to a cached prefix, against the oracle."""
+    from paper_2608_11742_amd._abi import KvCache
+    shape, w_np, model = tiny
+    prefix = synth.tokens_np(Pn, "prefix", Pn, shape.vocab - 1)
+    k, vt, cap = model.new_kv_cache(Pn)
+    kvc = KvCache(k.data_ptr(), vt.data_ptr(), 0, cap)
+    model.forward(torch.from_numpy(prefix).to(DEV)[None], torch.arange(1, dtype=torch.int32, device=DEV),
+                  kv_out=kvc)
+    kvc.len = Pn
+    shared, packed = _packed_case(shape, S, 0, B, n, seed=Pn + S)
+    lm_pos = _lm_pos(S, 0, B)
+    scales = (1.0 + 6.0 * synth.uniform01_np(Pn + 1, "s", S)).astype(np.float32)
+    out = model.forward_packed(torch.from_numpy(packed).to(DEV), S, 0, B, n, torch.from_numpy(lm_pos).to(DEV),
+                               row_scale=torch.from_numpy(scales).to(DEV), scale=2.0, pos_offset=Pn, kv_prefix=kvc)
+    torch.cuda.synchronize()
+    kv = om.prefix_cache(prefix, w_np, shape)
+    logits = om.packed_logits(packed, w_np, shape, S, 0, B, n, lm_pos, pos_offset=Pn, row_scale=scales[lm_pos],
+                              scale=2.0, prefix_kv=kv)
+    ref = softmax_stats(logits.reshape(-1, shape.vocab), 16)
+    print(compare_stats(out.numpy(), ref, 1e-4, label=f"packed over prefix {Pn}: S{S} B{B} n{n}"))
+
+
+@pytest.mark.parametrize("tau_pivot,lam,seed", [(0.9, 0.1, 21), (0.6, 0.3, 22)])
+def test_packed_cached_decode_trajectory_matches_oracle(P, tiny, tau_pivot, lam, seed):
+    from oracle.decode import model_prefix_cached
+    shape, w_np, model = tiny
+    Pl, G, B = 16, 96, 32
+    prompt = synth.tokens_np(seed, "prompt", Pl, shape.vocab - 1)
+    scales = synth.position_scales_np(seed + 10, np.arange(Pl + G), 2.6, 16.0)
+    prm = P.params(mode="paper", k_max=10, tau_pivot=tau_pivot, n_pivots=1, r=0.1, n_cand=10, max_branch=15)
+    toks, st = P.rps_decode(model, torch.from_numpy(prompt).to(DEV), G, B, prm, lam, 0.9, capacity=16,
+                            row_scale=torch.from_numpy(scales).to(DEV), record=True, packed=True, prefix_cache=True)
+    got = toks.cpu().numpy()
+    oprm = orps.Params(mode="paper", k_max=10, tau_pivot=tau_pivot, r=0.1, n_cand=10)
+    ref = oracle_decode(model_forward(w_np, shape, scales=scales), prompt, G, B, shape.mask_id, oprm, lam, 0.9,
+                        capacity=16, block_forward=model_prefix_cached(w_np, shape, scales=scales, packed=True))
+    excluded = None
+    for i, (g, o) in enumerate(zip(st.trace, ref.trace)):
+        if tuple(g) != tuple(_event_key(o)):
+            assert o[-1] <= MARGIN, f"event {i}: gpu {g} vs oracle {o}"
+            excluded = i
+            break
+    if excluded is None:
+        assert len(st.trace) == len(ref.trace)
+        assert np.array_equal(got, ref.tokens)
+        assert st.nfe == ref.nfe and st.lookahead == ref.lookahead
+    assert np.all(got[Pl:] != shape.mask_id)
+    assert st.lookahead > 0
+    print(f"packed + prefix cache: nfe {st.nfe} (lookahead {st.lookahead}), pivot commits {st.commits_pivot}, "
+          f"abstains {st.abstains}, first excluded event {excluded}")
