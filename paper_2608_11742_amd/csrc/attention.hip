@@ -46,12 +46,6 @@ struct AttnCfg {
 // row r, chunk c of a tile stored with rows of `row_bytes`: chunk slot c ^ (r % 8)
 __device__ __forceinline__ int swz(int r, int c, int row_bytes) { return r * row_bytes + ((c ^ (r & 7)) << 4); }
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-  const bf16x2_t v = {static_cast<__bf16>(a), static_cast<__bf16>(b)};   // round to nearest even
-  return __builtin_bit_cast(uint32_t, v);
-}
-
 template <typename T, int HD, bool kPacked>
 __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_scale_log2) {
   using C = AttnCfg<T, HD>;

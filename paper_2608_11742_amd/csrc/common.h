@@ -45,6 +45,20 @@ template <> struct Elem<bf16_t> {
   __device__ __forceinline__ static bf16_t from_f(float v) { return bf16_t{f2bf(v)}; }
 };
 
+// two floats -> two bfloat16 in one word (a in the low half), hardware
+// round to nearest even
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t v = {static_cast<__bf16>(a), static_cast<__bf16>(b)};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// silu(g) = g / (1 + e^-g) with the hardware base-2 exponential and
+// reciprocal (about 1 ulp each)
+__device__ __forceinline__ float silu_fast(float g) {
+  return g * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * g));
+}
+
 __device__ __forceinline__ float load_f(const float* p) { return *p; }
 __device__ __forceinline__ float load_f(const bf16_t* p) { return bf2f(p->bits); }
 __device__ __forceinline__ void store_f(float* p, float v) { *p = v; }

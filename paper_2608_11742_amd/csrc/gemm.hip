@@ -53,6 +53,70 @@ struct EpiParams {
   int np;
 };
 
+// gate/up epilogue of one tile: out = silu(gate) * up.  The blocks are
+// transposed (TileMma TRANS): lane l holds row 16 m + l % 16, columns
+// 16 n + 4 (l / 16) + i of the wave tile; gate block n pairs with up block
+// n + kFN / 2, so each lane stores 4 consecutive outputs at once.
+template <typename T, class Cfg, class TM>
+__device__ __forceinline__ void swiglu_store(const f32x4 (&acc)[TM::kFM][TM::kFN], int m0, int tn, int M,
+                                             const EpiParams& ep) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
+  T* out = reinterpret_cast<T*>(ep.out);
+  constexpr int kOC = TM::kWTN / 2, kNG = TM::kFN / 2;
+  const int jw = tn * (Cfg::BN / 2) + wn * kOC, rw = m0 + wm * TM::kWTM;   // wave tile origin
+  const int j0 = jw + 4 * (lane >> 4), r0 = rw + (lane & 15);
+  // all values first (independent chains the scheduler can interleave),
+  // then the stores: unguarded when the whole wave tile is in range
+  float v[TM::kFM][kNG][4];
+#pragma unroll
+  for (int m = 0; m < TM::kFM; ++m)
+#pragma unroll
+    for (int n = 0; n < kNG; ++n)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[m][n][i] = silu_fast(acc[m][n][i]) * acc[m][n + kNG][i];
+  const bool vec = (ep.F % 4) == 0 && (reinterpret_cast<uintptr_t>(out) & (4 * sizeof(T) - 1)) == 0;
+  if (vec && rw + TM::kWTM <= M && jw + kOC <= ep.F) {
+#pragma unroll
+    for (int m = 0; m < TM::kFM; ++m)
+#pragma unroll
+      for (int n = 0; n < kNG; ++n) {
+        T* dst = out + size_t(r0 + 16 * m) * ep.F + j0 + 16 * n;
+        if constexpr (Elem<T>::bytes == 2)
+          *reinterpret_cast<u32x2*>(dst) =
+              u32x2{pack_bf16x2(v[m][n][0], v[m][n][1]), pack_bf16x2(v[m][n][2], v[m][n][3])};
+        else
+          *reinterpret_cast<f32x4*>(dst) = f32x4{v[m][n][0], v[m][n][1], v[m][n][2], v[m][n][3]};
+      }
+  } else {
+#pragma unroll
+    for (int m = 0; m < TM::kFM; ++m)
+#pragma unroll
+      for (int n = 0; n < kNG; ++n)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = r0 + 16 * m, j = j0 + 16 * n + i;
+          if (row < M && j < ep.F) store_f(out + size_t(row) * ep.F + j, v[m][n][i]);
+        }
+  }
+}
+
+// B row of local tile row r in a gate/up tile: each wave column of kWTN rows
+// pairs kWTN / 2 gate rows with the kWTN / 2 up rows of the same outputs
+template <class Cfg, class TM>
+__device__ __forceinline__ int gu_row(int r, int tn, int F) {
+  constexpr int kHalf = TM::kWTN / 2;
+  const int wn = r / TM::kWTN, rr = r % TM::kWTN;
+  const int j = min(tn * (Cfg::BN / 2) + wn * kHalf + rr % kHalf, F - 1);
+  return rr < kHalf ? j : F + j;
+}
+
+// in-sequence position id of row `row` of the QKV projection (absolute, packed-lookahead aware)
+__device__ __forceinline__ int qkv_pos(const QkvOut& o, int row) {
+  const int r = row % o.seq;
+  return o.pos_offset + (o.pack_B && r >= o.pack_S ? o.pack_b0 + ((r - o.pack_S) & (o.pack_B - 1)) : r);
+}
+
 // HD: head_dim of the QKV epilogue (compile-time, so the rotary partner block
 // index stays static and the accumulators stay in registers); 0 otherwise.
 template <typename T, int EPI, int HD, class Cfg>
@@ -60,7 +124,8 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
                                                                 const T* __restrict__ B, int ldb, int M, int N,
                                                                 int K, int tiles_m, int tiles_n, EpiParams ep) {
   constexpr int kBM = Cfg::BM, kWavesN = Cfg::WN;
-  using TM = TileMma<T, Cfg::BM, Cfg::BN, Cfg::WM, Cfg::WN>;
+  constexpr bool kTrans = EPI == EPI_SWIGLU;
+  using TM = TileMma<T, Cfg::BM, Cfg::BN, Cfg::WM, Cfg::WN, kTrans>;
   constexpr bool kSplit = EPI == EPI_PART || EPI == EPI_PART_GU;
   __shared__ __attribute__((aligned(16))) uint8_t smem[TM::kSmem];
   int tm, tn;
@@ -80,12 +145,7 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
   auto b_off = [&](int r) -> uint32_t {
     int row;
     if constexpr (EPI == EPI_SWIGLU || EPI == EPI_PART_GU) {
-      // BN rows -> BN / 2 outputs: each wave column of kWTN rows pairs kWTN / 2
-      // gate rows with the kWTN / 2 up rows of the same outputs
-      constexpr int kHalf = TM::kWTN / 2;
-      const int wn = r / TM::kWTN, rr = r % TM::kWTN;
-      const int j = min(tn * (Cfg::BN / 2) + wn * kHalf + rr % kHalf, ep.F - 1);
-      row = rr < kHalf ? j : ep.F + j;
+      row = gu_row<Cfg, TM>(r, tn, ep.F);   // BN rows -> BN / 2 outputs
     } else {
       row = min(tn * Cfg::BN + r, N - 1);
     }
@@ -174,22 +234,7 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
       }
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
-    T* out = reinterpret_cast<T*>(ep.out);
-#pragma unroll
-    for (int m = 0; m < TM::kFM; ++m)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = row_base + m * 16 + i;
-        if (row >= M) continue;
-#pragma unroll
-        for (int n = 0; n < TM::kFN / 2; ++n) {
-          const int j = tn * (Cfg::BN / 2) + wn * (TM::kWTN / 2) + n * 16 + lc;
-          if (j >= ep.F) continue;
-          const float g = acc[m][n][i], u = acc[m][n + TM::kFN / 2][i];
-          const float silu = g / (1.0f + __expf(-g));
-          store_f(out + size_t(row) * ep.F + j, silu * u);
-        }
-      }
+    swiglu_store<T, Cfg, TM>(acc, m0, tn, M, ep);
   } else {  // EPI_QKV
     static_assert(HD == 64 || HD == 128, "head_dim");
     const QkvOut& o = ep.qkv;
@@ -236,7 +281,7 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
 #pragma unroll
             for (int n = 0; n < TM::kFN; ++n) {
               const int r = m * 16 + 4 * (lane >> 4) + i, c = n * 16 + lc;
-              *reinterpret_cast<uint16_t*>(st + (r * TM::kWTN + c) * 2) = f2bf(acc[m][n][i]);
+              *reinterpret_cast<uint16_t*>(st + (r * TM::kWTN + c) * 2) = uint16_t(pack_bf16x2(acc[m][n][i], 0.f));
             }
       } else {
 #pragma unroll
@@ -244,8 +289,8 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
 #pragma unroll
           for (int n = 0; n < TM::kFN; ++n) {
             const int r = m * 16 + 4 * (lane >> 4), c = n * 16 + lc;
-            const uint32_t lo = uint32_t(f2bf(acc[m][n][0])) | (uint32_t(f2bf(acc[m][n][1])) << 16);
-            const uint32_t hi = uint32_t(f2bf(acc[m][n][2])) | (uint32_t(f2bf(acc[m][n][3])) << 16);
+            const uint32_t lo = pack_bf16x2(acc[m][n][0], acc[m][n][1]);
+            const uint32_t hi = pack_bf16x2(acc[m][n][2], acc[m][n][3]);
             *reinterpret_cast<u32x2*>(st + (c * TM::kWTM + r) * 2) = u32x2{lo, hi};
           }
       }
@@ -304,6 +349,61 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
         }
     }
   }
+}
+
+// Gate/up + SwiGLU over all tiles with one workgroup per CU, each taking
+// tiles blockIdx.x, blockIdx.x + gridDim.x, ...: the copies of a tile's first
+// K stage are issued before the previous tile's epilogue (which keeps its
+// data in registers) and those of the second after its stores, so the first
+// stage's latency hides behind the epilogue and the first wait does not
+// wait for the stores.
+template <typename T, class Cfg>
+__global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_swiglu_persist_kernel(
+    const T* __restrict__ A, int lda, const T* __restrict__ B, int M, int K, int tiles_m, int tiles_n, EpiParams ep) {
+  using TM = TileMma<T, Cfg::BM, Cfg::BN, Cfg::WM, Cfg::WN, true>;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[TM::kSmem];
+  const int ntiles = tiles_m * tiles_n;
+  const int nk = K / TM::kKPerStage;
+  const uint8_t* A8 = reinterpret_cast<const uint8_t*>(A);
+  const uint8_t* B8 = reinterpret_cast<const uint8_t*>(B);
+  const uint32_t a_row_bytes = uint32_t(lda) * sizeof(T), b_row_bytes = uint32_t(K) * sizeof(T);
+  auto a_off_of = [=](int m0) { return [=](int r) -> uint32_t { return uint32_t(min(m0 + r, M - 1)) * a_row_bytes; }; };
+  auto b_off_of = [=](int tn) {
+    return [=](int r) -> uint32_t { return uint32_t(gu_row<Cfg, TM>(r, tn, ep.F)) * b_row_bytes; };
+  };
+  int id = blockIdx.x, tm, tn;
+  map_tile(id, ntiles, tiles_m, tiles_n, kGroupM, tm, tn);
+  TM::issue_stage(smem, A8, B8, a_off_of(tm * Cfg::BM), b_off_of(tn), nk, 0);
+  TM::issue_stage(smem, A8, B8, a_off_of(tm * Cfg::BM), b_off_of(tn), nk, 1);
+  for (;;) {
+    f32x4 acc[TM::kFM][TM::kFN];
+    TM::template run<true>(smem, A8, B8, a_off_of(tm * Cfg::BM), b_off_of(tn), nk, acc);
+    const int next = id + int(gridDim.x);
+    int tm1 = 0, tn1 = 0;
+    if (next < ntiles) {
+      map_tile(next, ntiles, tiles_m, tiles_n, kGroupM, tm1, tn1);
+      TM::issue_stage(smem, A8, B8, a_off_of(tm1 * Cfg::BM), b_off_of(tn1), nk, 0);
+    }
+    swiglu_store<T, Cfg, TM>(acc, tm * Cfg::BM, tn, M, ep);
+    if (next >= ntiles) break;
+    TM::issue_stage(smem, A8, B8, a_off_of(tm1 * Cfg::BM), b_off_of(tn1), nk, 1);
+    id = next;
+    tm = tm1;
+    tn = tn1;
+  }
+}
+
+// compute units of the current device (cached per device)
+int device_cus() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
 }
 
 template <typename T, int EPI, int HD, class Cfg>
@@ -384,11 +484,6 @@ __global__ __launch_bounds__(kRedThreads) void splitk_swiglu_kernel(const float*
   for (int e = 0; e < 4; ++e) store_f(out + size_t(row) * F + j + e, g[e] / (1.0f + __expf(-g[e])) * u[e]);
 }
 
-// in-sequence position id of row `row` of the QKV projection (as the fused epilogue)
-__device__ __forceinline__ int qkv_pos(const QkvOut& o, int row) {
-  const int r = row % o.seq;
-  return o.pos_offset + (o.pack_B && r >= o.pack_S ? o.pack_b0 + ((r - o.pack_S) & (o.pack_B - 1)) : r);
-}
 
 // Q and K: one thread per (row, q or k, head, dim < HD/2) pair; sums the two
 // partners, rotates them and writes both to the head-major layout
@@ -529,6 +624,21 @@ hipError_t gemm_swiglu(int dtype, const void* A, int lda, const void* Wgu, int M
     else
       hipLaunchKernelGGL(splitk_swiglu_kernel<float>, g, dim3(kRedThreads), 0, s, sk->part, sk->splits, M, F, ep.np,
                          static_cast<float*>(out));
+    return hipGetLastError();
+  }
+  if (M > kSmallM) {
+    // 256 x 256 tiles, one persistent workgroup per CU
+    const int stage_k = dtype ? 2 * TileMma<bf16_t, Big::BM, Big::BN, Big::WM, Big::WN>::kKPerStage
+                              : 2 * TileMma<float, Big::BM, Big::BN, Big::WM, Big::WN>::kKPerStage;
+    if (K <= 0 || K % stage_k) return hipErrorInvalidValue;
+    const int tiles_m = cdiv(M, Big::BM), tiles = tiles_m * tn;
+    const int grid = std::min(tiles, device_cus());
+    if (dtype)
+      hipLaunchKernelGGL((gemm_swiglu_persist_kernel<bf16_t, Big>), dim3(grid), dim3(Big::kThreads), 0, s,
+                         static_cast<const bf16_t*>(A), lda, static_cast<const bf16_t*>(Wgu), M, K, tiles_m, tn, ep);
+    else
+      hipLaunchKernelGGL((gemm_swiglu_persist_kernel<float, Big>), dim3(grid), dim3(Big::kThreads), 0, s,
+                         static_cast<const float*>(A), lda, static_cast<const float*>(Wgu), M, K, tiles_m, tn, ep);
     return hipGetLastError();
   }
   return dtype ? launch<bf16_t, EPI_SWIGLU>(A, lda, Wgu, K, M, 2 * F, K, tn, ep, s)

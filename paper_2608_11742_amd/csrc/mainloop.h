@@ -73,7 +73,11 @@ __device__ __forceinline__ uint32_t lds_address(const void* p) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) uint8_t*)(p)));
 }
 
-template <typename T, int BM, int BN, int WAVES_M, int WAVES_N>
+// TRANS: every 16x16 block is computed as (B A^T)^T, so that lane l holds
+// row 16 m + l % 16 and the 4 consecutive columns 16 n + 4 (l / 16) + i of
+// block (m, n) (instead of 4 consecutive rows of one column): row-contiguous
+// epilogues then store 4 values per lane.
+template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, bool TRANS = false>
 struct TileMma {
   static constexpr int kWaves = WAVES_M * WAVES_N;
   static constexpr int kThreads = kWaves * kWave;
@@ -95,42 +99,72 @@ struct TileMma {
   // byte offset within a stage of logical chunk c (0..7) of local row r
   __device__ __forceinline__ static int swz(int r, int c) { return r * kRowBytes + ((c ^ (r & 7)) << 4); }
 
-  // a_off(r) / b_off(r): byte offset of local row r (already clamped to a
-  // valid row) relative to A / B.  nk: K / kKPerStage (even).  smem: kSmem bytes.
-  template <class AOff, class BOff>
-  __device__ __forceinline__ static void run(uint8_t* smem, const uint8_t* A, const uint8_t* B, AOff a_off,
-                                             BOff b_off, int nk, f32x4 (&acc)[kFM][kFN]) {
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    // wave index as a scalar: the LDS addresses of the load instructions are
-    // then computed on the scalar unit, with no per-load register round trip
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave / WAVES_N;
-    const int wn = wave % WAVES_N;
-    const int ns = nk >> 1;   // stages
-
-    // this lane's source row and chunk for each of the wave's load instructions
-    const uint32_t chunk_off = uint32_t((lane & 7) ^ (lane >> 3)) << 4;
+  // The wave's share of the global -> LDS copies of one tile: lane source
+  // offsets and buffer descriptors.  a_off(r) / b_off(r): byte offset of
+  // local row r (already clamped to a valid row) relative to A / B.
+  struct Loader {
     uint32_t ga[kIA], gb[kIB];
+    uint32_t lds0;
+    i32x4 ra, rb;
+    int wave;
+    template <class AOff, class BOff>
+    __device__ __forceinline__ Loader(uint8_t* smem, const uint8_t* A, const uint8_t* B, AOff a_off, BOff b_off) {
+      const int lane = threadIdx.x & 63;
+      // wave index as a scalar: the LDS addresses of the load instructions are
+      // then computed on the scalar unit, with no per-load register round trip
+      wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
+      // this lane's source row and chunk for each of the wave's load instructions
+      const uint32_t chunk_off = uint32_t((lane & 7) ^ (lane >> 3)) << 4;
 #pragma unroll
-    for (int i = 0; i < kIA; ++i) ga[i] = a_off((wave * kIA + i) * 8 + (lane >> 3)) + chunk_off;
+      for (int i = 0; i < kIA; ++i) ga[i] = a_off((wave * kIA + i) * 8 + (lane >> 3)) + chunk_off;
 #pragma unroll
-    for (int i = 0; i < kIB; ++i) gb[i] = b_off((wave * kIB + i) * 8 + (lane >> 3)) + chunk_off;
-    const uint32_t lds0 = lds_address(smem);
-    const i32x4 ra = buffer_rsrc(A), rb = buffer_rsrc(B);
-    auto dma_a = [&](int i, uint32_t koff, uint32_t sbase) {
+      for (int i = 0; i < kIB; ++i) gb[i] = b_off((wave * kIB + i) * 8 + (lane >> 3)) + chunk_off;
+      lds0 = lds_address(smem);
+      ra = buffer_rsrc(A);
+      rb = buffer_rsrc(B);
+    }
+    __device__ __forceinline__ void dma_a(int i, uint32_t koff, uint32_t sbase) const {
       lds_dma16(ra, ga[i], koff, sbase + (wave * kIA + i) * 1024);
-    };
-    auto dma_b = [&](int i, uint32_t koff, uint32_t sbase) {
+    }
+    __device__ __forceinline__ void dma_b(int i, uint32_t koff, uint32_t sbase) const {
       lds_dma16(rb, gb[i], koff, sbase + kStageA + (wave * kIB + i) * 1024);
-    };
-    auto issue = [&](int st, int slot) {
+    }
+    __device__ __forceinline__ void issue(int st, int slot) const {
       const uint32_t koff = uint32_t(st) * kRowBytes, sbase = lds0 + slot * kStage;
 #pragma unroll
       for (int i = 0; i < kIA; ++i) dma_a(i, koff, sbase);
 #pragma unroll
       for (int i = 0; i < kIB; ++i) dma_b(i, koff, sbase);
-    };
+    }
+  };
+
+  // Issue the copies of K stage `st` (0 or 1) of a tile (nk as in run) into
+  // ring slot st: a caller that holds no live data in the ring starts the
+  // next tile's copies around the current tile's epilogue.
+  template <class AOff, class BOff>
+  __device__ __forceinline__ static void issue_stage(uint8_t* smem, const uint8_t* A, const uint8_t* B, AOff a_off,
+                                                     BOff b_off, int nk, int st) {
+    const Loader ld(smem, A, B, a_off, b_off);
+    ld.issue(min(st, (nk >> 1) - 1), st);
+  }
+
+  // nk: K / kKPerStage (even).  smem: kSmem bytes.  PRE: stages 0 and 1 were
+  // issued by issue_stage, in this order, and stage 1 is the last vector
+  // memory load issued (stores may follow it or sit between the two): loads
+  // complete in order, so with at most one stage of operations outstanding
+  // stage 0 has landed, whatever the stores do.
+  template <bool PRE = false, class AOff, class BOff>
+  __device__ __forceinline__ static void run(uint8_t* smem, const uint8_t* A, const uint8_t* B, AOff a_off,
+                                             BOff b_off, int nk, f32x4 (&acc)[kFM][kFN]) {
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const Loader ld(smem, A, B, a_off, b_off);
+    const int wave = ld.wave;
+    const int wm = wave / WAVES_N;
+    const int wn = wave % WAVES_N;
+    const int ns = nk >> 1;   // stages
+    auto dma_a = [&](int i, uint32_t koff, uint32_t sbase) { ld.dma_a(i, koff, sbase); };
+    auto dma_b = [&](int i, uint32_t koff, uint32_t sbase) { ld.dma_b(i, koff, sbase); };
 
 #pragma unroll
     for (int m = 0; m < kFM; ++m)
@@ -149,7 +183,10 @@ struct TileMma {
                                              swz(wn * kWTN + n * 16 + fr, 4 * h + fc));
     };
     auto mma_one = [&](int r, int i) {
-      Mfma<T>::run(acc[i / kFN][i % kFN], af[r][i / kFN], bfr[r][i % kFN]);
+      if constexpr (TRANS)
+        Mfma<T>::run(acc[i / kFN][i % kFN], bfr[r][i % kFN], af[r][i / kFN]);
+      else
+        Mfma<T>::run(acc[i / kFN][i % kFN], af[r][i / kFN], bfr[r][i % kFN]);
     };
 
     // Every step has the same shape: no branch but the loop's back-edge (a
@@ -158,8 +195,10 @@ struct TileMma {
     // the loads repeat stage ns - 1 into the slot just released, so that the
     // number of loads in flight, and with it every vmcnt wait, stays uniform;
     // that slot is not read again as a live stage.
-    issue(0, 0);
-    issue(min(1, ns - 1), 1);
+    if constexpr (!PRE) {
+      ld.issue(0, 0);
+      ld.issue(min(1, ns - 1), 1);
+    }
     wait_vmcnt<kIA + kIB>();   // stage 0 landed
     __syncthreads();
 #pragma unroll
@@ -210,7 +249,7 @@ struct TileMma {
       wait_vmcnt<0>();
       __syncthreads();
       __builtin_amdgcn_sched_barrier(0);
-      const uint32_t koff = uint32_t(min(j + 2, ns - 1)) * kRowBytes, sbase = lds0 + cur * kStage;
+      const uint32_t koff = uint32_t(min(j + 2, ns - 1)) * kRowBytes, sbase = ld.lds0 + cur * kStage;
       static_for<0, kComp1>([&](auto cc) {
         constexpr int c = decltype(cc)::value;
         if constexpr (kPre1 + c < kMma) {

@@ -21,8 +21,12 @@ def determined_ranks(ref_logits: np.ndarray, kth_margin: np.ndarray, margin: flo
     return (gaps > margin) & (left > margin)
 
 
-def compare_stats(got: dict, ref, tol: float, k: int | None = None, margin=MARGIN, label: str = ""):
+def compare_stats(got: dict, ref, tol: float, k: int | None = None, margin=MARGIN, label: str = "",
+                  logit_tol: float | None = None):
     """Float fields within tol (max-abs); argmax and top-k ids equal where determined.
+
+    logit_tol (default tol) bounds the individual logits (lmax, top-k
+    logits); entropies and log-partition values keep tol.
 
     margin="auto" (end-to-end bf16 comparisons, where the inputs of the LM head
     already differ by rounding-order effects amplified through the layers):
@@ -31,15 +35,17 @@ def compare_stats(got: dict, ref, tol: float, k: int | None = None, margin=MARGI
     on identical inputs use the fixed 1e-3.
     """
     k = k or ref.topk_id.shape[1]
+    logit_tol = tol if logit_tol is None else logit_tol
     report = {}
     for name in ("H", "lse", "lmax"):
         err = float(np.max(np.abs(got[name].astype(np.float64) - getattr(ref, name))))
         report[name] = err
-        assert err <= tol, f"{label} {name}: max-abs error {err:.3e} > {tol:.1e}"
+        bound = logit_tol if name == "lmax" else tol
+        assert err <= bound, f"{label} {name}: max-abs error {err:.3e} > {bound:.1e}"
     # the r-th largest logit is defined even where tied tokens swap ranks
     tl_err = float(np.max(np.abs(got["topk_logit"][:, :k] - ref.topk_logit[:, :k])))
     report["topk_logit"] = tl_err
-    assert tl_err <= tol, f"{label} topk_logit: max-abs error {tl_err:.3e} > {tol:.1e}"
+    assert tl_err <= logit_tol, f"{label} topk_logit: max-abs error {tl_err:.3e} > {logit_tol:.1e}"
     if margin == "auto":
         margin = max(MARGIN, 2.0 * max(tl_err, report["lmax"]))
     report["margin"] = margin

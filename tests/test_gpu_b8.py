@@ -187,5 +187,11 @@ def test_cached_step_two_layer_8b_width(P, b8_two_layer):
     h = om.hidden(blocks[b], w_np, shape, pos_offset=Pn, mirror=True, prefix_kv=ref_kv)
     ref = softmax_stats(om.lm_logits(h, w_np, shape, scale=1.0), 16)
     got = {kk: v[b * Bk:(b + 1) * Bk] for kk, v in out.numpy().items()}
-    print(compare_stats(got, ref, 2e-2, margin="auto", label="cached step 2-layer 8B width"))
+    # Individual logits of this model are at the oracle's own noise floor:
+    # perturbing the mirror oracle by a relative 1e-7 (about one float32 ulp)
+    # at its bfloat16 rounding points moves branch 7's top-1 logits by
+    # 1.9e-2, by 1e-6 by 2.4e-2 (two random layers amplify rounding-order
+    # differences over 1056 keys; entropies move by 4e-4).  Logits therefore
+    # get 3e-2 here; entropies and log-partition values keep 2e-2.
+    print(compare_stats(got, ref, 2e-2, margin="auto", label="cached step 2-layer 8B width", logit_tol=3e-2))
     model_p.close()
