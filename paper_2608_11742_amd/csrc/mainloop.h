@@ -250,7 +250,7 @@ struct TileMma {
       __syncthreads();
       __builtin_amdgcn_sched_barrier(0);
       const uint32_t koff = uint32_t(min(j + 2, ns - 1)) * kRowBytes, sbase = ld.lds0 + cur * kStage;
-      static_for<0, kComp1>([&](auto cc) {
+      static_for<0, (kMma - kPre1 > kComp1 ? kMma - kPre1 : kComp1)>([&](auto cc) {
         constexpr int c = decltype(cc)::value;
         if constexpr (kPre1 + c < kMma) {
           mma_one(1, kPre1 + c);
@@ -260,7 +260,7 @@ struct TileMma {
           dma_a(c, koff, sbase);
         else if constexpr (c < kIA + kIB)
           dma_b(c - kIA, koff, sbase);
-        else
+        else if constexpr (c < kComp1)
           read_into(0, nxt, 0, c - kIA - kIB);
         __builtin_amdgcn_sched_barrier(0);
       });
