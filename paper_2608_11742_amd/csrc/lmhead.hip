@@ -83,11 +83,12 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_kernel(const T* __restrict
   constexpr int kSegs = Cfg::kSegs, kRowStride = Cfg::kRowStride;
   __shared__ __attribute__((aligned(16))) uint8_t smem[Cfg::kSmem];
 
-  // XCD-contiguous ids; all row tiles of one vocabulary slice run on one XCD
-  const int nwg = gridDim.x, id = blockIdx.x;
-  const int q = nwg / 8, rr = nwg % 8, xcd = id % 8, local = id / 8;
-  const int lin = xcd < rr ? xcd * (q + 1) + local : rr * (q + 1) + (xcd - rr) * q + local;
-  const int slice = lin / row_tiles, rt = lin % row_tiles;
+  // XCD-contiguous ids, walked in groups of 8 row tiles: the 32 workgroups an
+  // XCD runs at a time cover 8 row tiles x 4 vocabulary slices, so each step
+  // of their vocabulary loops fetches 12 operand panels into that XCD's L2
+  // (16 row tiles x 2 slices would fetch 18)
+  int rt, slice;
+  map_tile(blockIdx.x, gridDim.x, row_tiles, n_slices, 8, rt, slice);
   const int t_begin = int((long long)slice * vtiles / n_slices);
   const int t_end = int((long long)(slice + 1) * vtiles / n_slices);
   const int m0 = rt * BM;
