@@ -46,6 +46,37 @@ struct AttnCfg {
 // row r, chunk c of a tile stored with rows of `row_bytes`: chunk slot c ^ (r % 8)
 __device__ __forceinline__ int swz(int r, int c, int row_bytes) { return r * row_bytes + ((c ^ (r & 7)) << 4); }
 
+// K tiles (bf16): chunk c of key row r in slot c ^ kswz(r).  An S^T block
+// reads the 16 rows 8 q + 4 kk + j (q, j < 4, see key_of); this swizzle maps
+// them to 16 distinct slots with 16 chunks per row (8 with 8), so the 16
+// lanes of a read touch distinct LDS banks.  fp32 tiles read 16 consecutive
+// rows: r % 8, as for V^T.
+// max / sum over lanes l, l ^ 16, l ^ 32, l ^ 48 (the four 16-lane groups
+// that hold one query's scores): two permlane swaps on the vector ALU
+// instead of two LDS permutes
+__device__ __forceinline__ float group4_max(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float u = __uint_as_float(a[0]), v = __uint_as_float(a[1]);
+  const float m = u > v ? u : v;
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+  const float p = __uint_as_float(b[0]), q = __uint_as_float(b[1]);
+  return p > q ? p : q;
+}
+__device__ __forceinline__ float group4_sum(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float m = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+template <typename T, int CK>
+__device__ __forceinline__ int kswz(int r) {
+  if constexpr (Elem<T>::per_chunk == 8)
+    return CK >= 16 ? ((r & 3) | (((r >> 3) & 3) << 2)) : ((r & 3) | (((r >> 3) & 1) << 2));
+  else
+    return r & 7;
+}
+
 template <typename T, int HD, bool kPacked>
 __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_scale_log2) {
   using C = AttnCfg<T, HD>;
@@ -102,6 +133,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
                                                    (4 * st + g) * 16);
   }
 
+  // Key (within the tile) of row r of S^T block kk in half h.  bf16: the
+  // rows of a 32-key half are gathered so that S^T output element i of lane
+  // group g in block kk is key 32 h + 8 g + 4 kk + i: each lane's 8
+  // probabilities of the half are 8 consecutive keys, i.e. one 16-byte chunk
+  // of a V^T row (the P V operand).  fp32 (4 keys per chunk): plain order.
+  auto key_of = [](int h, int kk, int r) {
+    if constexpr (Elem<T>::per_chunk == 8) return 32 * h + 8 * (r >> 2) + 4 * kk + (r & 3);
+    else return 32 * h + 16 * kk + r;
+  };
   const uint32_t lds0 = lds_address(smem);
   // key range of tile t: source, first key, number of valid keys of the source, V^T row pitch
   struct Src {
@@ -129,7 +169,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
 #pragma unroll
     for (int i = 0; i < C::IK; ++i) {
       const int grp = wave * C::IK + i;
-      const int r = grp * C::RK + lane / C::CK, c = (lane % C::CK) ^ (r & 7);
+      const int r = grp * C::RK + lane / C::CK, c = (lane % C::CK) ^ kswz<T, C::CK>(r);
       const int key = min(s.k0 + r, s.nk - 1);
       lds_dma16(rk, uint32_t(key) * (HD * Elem<T>::bytes) + c * 16, 0, base + grp * 1024);
     }
@@ -196,11 +236,11 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
       f32x4 sc[2][2];
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
-        const int kb = 2 * half + kk;
         sc[kk][0] = sc[kk][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int st = 0; st < C::QSTEPS; ++st) {
-          const u32x4 kf = *reinterpret_cast<const u32x4*>(s + swz(kb * 16 + fr, 4 * st + g, C::CK * 16));
+          const int kr = key_of(half, kk, fr);
+          const u32x4 kf = *reinterpret_cast<const u32x4*>(s + kr * (C::CK * 16) + (((4 * st + g) ^ kswz<T, C::CK>(kr)) << 4));
           Mfma<T>::run(sc[kk][0], kf, qf[0][st]);
           Mfma<T>::run(sc[kk][1], kf, qf[1][st]);
         }
@@ -212,22 +252,36 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
         float mt = -INFINITY;
+        if (full) {   // wave-uniform: no key of this half is masked
+#pragma unroll
+          for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              p[kk][qb][i] = sc[kk][qb][i];
+              mt = fmaxf(mt, sc[kk][qb][i]);
+            }
+        } else {
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const int key = k0 + (2 * half + kk) * 16 + 4 * g + i;
+            const int key = k0 + key_of(half, kk, 4 * g + i);
             bool ok = key < nk;
             if (pmask)
               ok = ok && (sr.branch >= 0 ? qbr[qb] == sr.branch
                                          : (qbr[qb] < 0 || key < a.pack_b0 || key >= a.pack_b0 + a.pack_B));
-            const float v = (full || ok) ? sc[kk][qb][i] : -INFINITY;
+            const float v = ok ? sc[kk][qb][i] : -INFINITY;
             p[kk][qb][i] = v;
             mt = fmaxf(mt, v);
           }
-        mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-        mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-        float mnew = fmaxf(mrun[qb], mt * qk_scale_log2);
+        }
+        mt = group4_max(mt);
+        // The exponent reference moves only when a score exceeds it by more
+        // than 8 (log2 units): probabilities stay below 2^8, o and l share the
+        // reference so o / l is unchanged, and the accumulators are rescaled
+        // rarely instead of at nearly every new maximum.
+        const float mcand = mt * qk_scale_log2;
+        float mnew = mcand > mrun[qb] + 8.f ? mcand : mrun[qb];
         // packed: a branch query can meet a tile whose keys it all masks
         // before any key it sees; exponents then use 0 and give 0, not NaN
         if constexpr (kPacked) mnew = mnew == -INFINITY ? 0.f : mnew;
@@ -270,11 +324,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
           }
 #pragma unroll
         for (int db = 0; db < C::NDB; ++db) {
-          const int r = db * 16 + fr;
-          const int ka = 32 * half + 4 * g, kbk = ka + 16;   // key offsets of the two 4-key halves
-          const u32x2 lo = *reinterpret_cast<const u32x2*>(sv + swz(r, ka >> 3, C::CV * 16) + (ka & 7) * 2);
-          const u32x2 hi = *reinterpret_cast<const u32x2*>(sv + swz(r, kbk >> 3, C::CV * 16) + (kbk & 7) * 2);
-          const u32x4 vf = u32x4{lo[0], lo[1], hi[0], hi[1]};
+          // this lane's 8 probabilities are keys 32 half + 8 g .. + 7 (see key_of)
+          const u32x4 vf = *reinterpret_cast<const u32x4*>(sv + swz(db * 16 + fr, 4 * half + g, C::CV * 16));
 #pragma unroll
           for (int qb = 0; qb < 2; ++qb) {
             Mfma<T>::run(o[db][qb], vf, pb[qb]);
@@ -311,9 +362,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
   // normalise and store O[b * Sq + q][h * HD + dim]
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
-    float l = lrun[qb];
-    l += __shfl_xor(l, 16, 64);
-    l += __shfl_xor(l, 32, 64);
+    const float l = group4_sum(lrun[qb]);
     const float inv = 1.0f / l;
     const int q = q0 + qb * 16 + fr;
     if (q >= a.Sq) continue;
