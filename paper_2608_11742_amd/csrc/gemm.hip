@@ -270,10 +270,17 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
       __builtin_amdgcn_sched_barrier(0);
     }
     if constexpr (Elem<T>::bytes == 2) {
-      // stage the wave's 64 x 128 tile as bf16 in LDS (V transposed), then write
-      // 16-byte chunks: Q/K rows are contiguous along head_dim, V^T rows along positions
-      uint8_t* st = smem + wave * (TM::kWTM * TM::kWTN * 2);
+      const int r0 = m0 + wm * TM::kWTM;
       if (which < 2) {
+        // Q, K: stage the wave's 64 x 128 bf16 tile in its own region of the
+        // idle ring (rows of 16 chunks; chunk c of row r in slot
+        // c ^ 2 ((r / 4) % 4), so the 4 row groups of a store hit different
+        // banks), then write 16-byte chunks along head_dim.  The wave reads
+        // back only what it wrote: its LDS operations complete in order, so
+        // no barrier.
+        static_assert(TM::kWTN == 128, "qkv staging: 16 chunks per row");
+        uint8_t* st = smem + wave * (TM::kWTM * TM::kWTN * 2);
+        auto off = [](int r, int c16) { return r * 256 + ((c16 ^ (((r >> 2) & 3) << 1)) << 4); };
 #pragma unroll
         for (int m = 0; m < TM::kFM; ++m)
 #pragma unroll
@@ -281,49 +288,41 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
 #pragma unroll
             for (int n = 0; n < TM::kFN; ++n) {
               const int r = m * 16 + 4 * (lane >> 4) + i, c = n * 16 + lc;
-              *reinterpret_cast<uint16_t*>(st + (r * TM::kWTN + c) * 2) = uint16_t(pack_bf16x2(acc[m][n][i], 0.f));
+              *reinterpret_cast<uint16_t*>(st + off(r, c >> 3) + (c & 7) * 2) = uint16_t(pack_bf16x2(acc[m][n][i], 0.f));
             }
-      } else {
-#pragma unroll
-        for (int m = 0; m < TM::kFM; ++m)
-#pragma unroll
-          for (int n = 0; n < TM::kFN; ++n) {
-            const int r = m * 16 + 4 * (lane >> 4), c = n * 16 + lc;
-            const uint32_t lo = pack_bf16x2(acc[m][n][0], acc[m][n][1]);
-            const uint32_t hi = pack_bf16x2(acc[m][n][2], acc[m][n][3]);
-            *reinterpret_cast<u32x2*>(st + (c * TM::kWTM + r) * 2) = u32x2{lo, hi};
-          }
-      }
-      __syncthreads();
-      const int r0 = m0 + wm * TM::kWTM;
-      if (which < 2) {
         uint16_t* dst = reinterpret_cast<uint16_t*>(which == 0 ? o.q : o.k);
-        for (int q = lane; q < TM::kWTM * TM::kWTN / 8; q += 64) {
-          const int r = q / (TM::kWTN / 8), c8 = (q % (TM::kWTN / 8)) * 8;
+#pragma unroll
+        for (int it = 0; it < TM::kWTM * TM::kWTN / 8 / 64; ++it) {
+          const int q = lane + 64 * it, r = q / 16, c16 = q % 16;
           const int row = r0 + r;
           if (row >= M) continue;
           const int b = row / o.seq, sp = row % o.seq;
-          const int cin = cin0 + c8, h = cin / hd, dim = cin % hd;
+          const int cin = cin0 + c16 * 8, h = cin / hd, dim = cin % hd;
           *reinterpret_cast<u32x4*>(dst + (size_t(b * o.H + h) * o.seq + sp) * hd + dim) =
-              *reinterpret_cast<const u32x4*>(st + (r * TM::kWTN + c8) * 2);
+              *reinterpret_cast<const u32x4*>(st + off(r, c16));
         }
       } else {
-        uint16_t* dst = reinterpret_cast<uint16_t*>(o.vt);
-        const bool aligned = (o.seq % 8) == 0;
-        for (int q = lane; q < TM::kWTM * TM::kWTN / 8; q += 64) {
-          const int c = q / (TM::kWTM / 8), rr = (q % (TM::kWTM / 8)) * 8;
-          const int cin = cin0 + c, h = cin / hd, dim = cin % hd;
-          const int row = r0 + rr;
+        // V^T: a lane's 4 values of a block are 4 consecutive positions of
+        // one head dim, i.e. 8 contiguous bytes of a V^T row: stored straight
+        // from registers (4 rows of one sequence when seq % 4 == 0)
+        uint16_t* vt = reinterpret_cast<uint16_t*>(o.vt);
+        const bool vec4 = (o.seq % 4) == 0 && (o.vt_ld % 4) == 0;
+#pragma unroll
+        for (int m = 0; m < TM::kFM; ++m) {
+          const int row = row_base + m * 16;   // rows row .. row + 3
           if (row >= M) continue;
-          if (aligned && row + 7 < M) {
-            const int b = row / o.seq, sp = row % o.seq;
-            *reinterpret_cast<u32x4*>(dst + (size_t(b * o.H + h) * hd + dim) * o.vt_ld + sp) =
-                *reinterpret_cast<const u32x4*>(st + (c * TM::kWTM + rr) * 2);
-          } else {
-            for (int e = 0; e < 8 && row + e < M; ++e) {
-              const int b = (row + e) / o.seq, sp = (row + e) % o.seq;
-              dst[(size_t(b * o.H + h) * hd + dim) * o.vt_ld + sp] =
-                  *reinterpret_cast<const uint16_t*>(st + (c * TM::kWTM + rr + e) * 2);
+          const int b = row / o.seq, sp = row - b * o.seq;
+#pragma unroll
+          for (int n = 0; n < TM::kFN; ++n) {
+            const int cin = cin0 + n * 16 + lc, h = cin / hd, dim = cin % hd;
+            if (vec4 && row + 3 < M) {
+              *reinterpret_cast<u32x2*>(vt + (size_t(b * o.H + h) * hd + dim) * o.vt_ld + sp) =
+                  u32x2{pack_bf16x2(acc[m][n][0], acc[m][n][1]), pack_bf16x2(acc[m][n][2], acc[m][n][3])};
+            } else {
+              for (int i = 0; i < 4 && row + i < M; ++i) {
+                const int bi = (row + i) / o.seq, si = (row + i) - bi * o.seq;
+                vt[(size_t(bi * o.H + h) * hd + dim) * o.vt_ld + si] = uint16_t(pack_bf16x2(acc[m][n][i], 0.f));
+              }
             }
           }
         }
