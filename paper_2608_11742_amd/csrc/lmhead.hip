@@ -6,8 +6,9 @@
 // the vocabulary.  For each 256-token vocabulary tile it runs the MFMA
 // mainloop, scales the logits, stages the 128x256 fp32 tile in LDS and lets
 // 4 threads per row scan 64 logits each, updating a running max m,
-// s = sum exp(l - m), t = sum exp(l - m) (l - m) and a sorted top-16 held in
-// registers.  At the end of its slice every thread writes its partial state.
+// s = sum exp(l - m), t = sum exp(l - m) (l - m) (m and t in log2 units
+// while scanning, natural units in the partials) and a sorted top-16.  At
+// the end of its slice every thread writes its partial state.
 // Pass 2 (merge_kernel): one workgroup per row merges all partials:
 //   M = max m_p, S = sum s_p e^(m_p - M), T = sum e^(m_p - M) (t_p + (m_p - M) s_p)
 //   lse = M + log S, H = log S - T / S, lmax = M,
@@ -27,6 +28,7 @@ constexpr int kK = DLLM_TOPK_REG;
 constexpr int kSegCols = 64;                             // logits per scan thread per pass
 constexpr int kSegStride = kSegCols * 4 + 16;            // padded segment bytes
 constexpr int kTargetWg = 512;
+constexpr float kLog2e = 1.4426950408889634f, kLn2 = 0.6931471805599453f;
 
 // BM rows per workgroup: 256 (8 waves of 64 x 128, the projection GEMMs'
 // tile) when there are more than 128 rows, else 128 (8 waves of 64 x 64).
@@ -157,9 +159,9 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_kernel(const T* __restrict
             d / TM::kKPerStage, acc);
     if constexpr (kListInMemory) {
       if (vt > t_begin && own_row) {
-        m = part.m[slot];
+        m = part.m[slot] * kLog2e;   // log2 units while scanning
         s = part.s[slot];
-        t = part.t[slot];
+        t = part.t[slot] * kLog2e;
 #pragma unroll
         for (int k = 0; k < kK; ++k) {
           tv[k] = part.tv[slot * kK + k];
@@ -192,11 +194,69 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_kernel(const T* __restrict
     }
     __syncthreads();
     // scan 64 logits of row srow: running statistics, and a bit mask of the
-    // logits that beat the pruning bound (candidates for the top 16)
+    // logits that may beat the pruning bound (candidates for the top 16)
     const uint8_t* base = smem + srow * kRowStride + sseg * kSegStride;
     const int c0 = n0 + pass * Cfg::kPassCols + sseg * kSegCols;
     const bool all_ok = c0 + kSegCols <= V && (mask_id < c0 || mask_id >= c0 + kSegCols);
+    if (vt == t_begin && pass == 0) {
+      // The slice's top-16 lists are still empty, which would make every
+      // logit a candidate.  Seed the bound instead: each thread takes the
+      // smallest of the maxima of its 8 groups of 8 logits (8 logits are at
+      // least that large), the row the smallest over its kSegs threads, so at
+      // least 16 logits of the row are at least as large as the bound and no
+      // smaller logit can reach the row's top 16.
+      float seed = INFINITY;
+#pragma unroll
+      for (int g8 = 0; g8 < kSegCols; g8 += 8) {
+        float gm = -INFINITY;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int col = c0 + g8 + e;
+          const float v = *reinterpret_cast<const float*>(base + (g8 + e) * 4) * rs_row;
+          if (all_ok || (col < V && col != mask_id)) gm = fmaxf(gm, v);
+        }
+        seed = fminf(seed, gm);
+      }
+#pragma unroll
+      for (int x = 1; x < kSegs; x <<= 1) seed = fminf(seed, __shfl_xor(seed, x, 64));
+      if (better(seed, 0x7fffffff, bv, bi)) {   // only ever raises the bound
+        bv = seed;
+        bi = 0x7fffffff;
+      }
+    }
     uint64_t cand = 0;
+    if (__all(all_ok)) {
+      // Every logit of the wave's segments is valid: branch-free scan in
+      // log2 units (x = logit * log2 e): one FMA, one exp2 and one FMA per
+      // logit; the reference max moves by selects.  Candidates are the
+      // logits with x at least the bound in log2 units less a relative
+      // 1e-6 (x and the bound round differently, by a few ulp at most), a
+      // superset of those that beat the bound; the insertion below checks
+      // each one exactly.
+      const float c2 = rs_row * kLog2e;
+      const float b2 = bv * kLog2e;
+      const float bv2 = own_row ? b2 - fabsf(b2) * 1e-6f : INFINITY;
+#pragma unroll
+      for (int c4 = 0; c4 < kSegCols; c4 += 4) {
+        const float4 v4 = *reinterpret_cast<const float4*>(base + c4 * 4);
+        const float x[4] = {v4.x * c2, v4.y * c2, v4.z * c2, v4.w * c2};
+        const float gmax = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+        const float mnew = fmaxf(m, gmax);
+        const float alpha = __builtin_amdgcn_exp2f(m - mnew);   // 1 if unchanged, 0 from -inf
+        const float d = alpha == 0.f ? 0.f : m - mnew;
+        t = alpha * (t + d * s);
+        s = alpha * s;
+        m = mnew;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float y = x[e] - m;
+          const float ex = __builtin_amdgcn_exp2f(y);
+          s += ex;
+          t = fmaf(ex, y, t);
+          cand |= uint64_t(x[e] >= bv2) << (c4 + e);
+        }
+      }
+    } else {
 #pragma unroll
     for (int c4 = 0; c4 < kSegCols; c4 += 4) {
       const float4 v4 = *reinterpret_cast<const float4*>(base + c4 * 4);
@@ -207,11 +267,11 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_kernel(const T* __restrict
       for (int e = 0; e < 4; ++e) {
         const int col = c0 + c4 + e;
         ok[e] = all_ok || (col < V && col != mask_id);
-        if (ok[e]) cmax = fmaxf(cmax, vv[e]);
+        if (ok[e]) cmax = fmaxf(cmax, vv[e] * kLog2e);
       }
-      if (cmax > m) {  // rescale the running sums to the new max
+      if (cmax > m) {  // rescale the running sums to the new max (log2 units)
         if (m > -INFINITY) {
-          const float alpha = fast_exp(m - cmax);
+          const float alpha = __builtin_amdgcn_exp2f(m - cmax);
           t = alpha * (t + (m - cmax) * s);
           s = alpha * s;
         }
@@ -220,12 +280,13 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_kernel(const T* __restrict
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         if (!ok[e]) continue;
-        const float x = vv[e] - m;
-        const float ex = fast_exp(x);
+        const float x = vv[e] * kLog2e - m;
+        const float ex = __builtin_amdgcn_exp2f(x);
         s += ex;
         t += ex * x;
         if (own_row && better(vv[e], c0 + c4 + e, bv, bi)) cand |= uint64_t(1) << (c4 + e);
       }
+    }
     }
     // insert the candidates; the wave loops as often as its busiest lane has candidates
     while (__any(cand != 0)) {
@@ -240,9 +301,9 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_kernel(const T* __restrict
     }
     if constexpr (!kListInMemory) refresh_bound();
     if (kListInMemory && own_row) {
-      part.m[slot] = m;
+      part.m[slot] = m * kLn2;   // natural units in the partials
       part.s[slot] = s;
-      part.t[slot] = t;
+      part.t[slot] = t * kLn2;
 #pragma unroll
       for (int k = 0; k < kK; ++k) {
         part.tv[slot * kK + k] = tv[k];
@@ -251,9 +312,9 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_kernel(const T* __restrict
     }
   }
   if (own_row && !kListInMemory) {
-    part.m[slot] = m;
+    part.m[slot] = m * kLn2;
     part.s[slot] = s;
-    part.t[slot] = t;
+    part.t[slot] = t * kLn2;
     {
 #pragma unroll
       for (int k = 0; k < kK; ++k) {
