@@ -3,7 +3,11 @@
 // (shared by all sequences of the batch).
 //
 // A workgroup of 4 waves takes 128 queries of one (sequence, head); each
-// wave owns 32 queries, two workgroups share a CU.  Keys stream through a
+// wave owns 32 queries, two workgroups share a CU.  Short sequences (at most
+// 64 queries, e.g. a block recomputed over a cached prefix) take 32 queries
+// per workgroup instead: wave w owns the 16 queries of block w % 2 and the
+// keys of half w / 2 of every tile, and the two halves' softmax states are
+// merged at the end, so no wave computes clamped duplicate queries.  Keys stream through a
 // two-slot LDS ring in tiles of 64 (K rows and V^T columns), copied from
 // global memory straight into LDS with buffer_load ... lds one tile ahead.
 // Scores are computed transposed, S^T = K Q^T, so in the MFMA output layout
@@ -24,6 +28,7 @@ constexpr int kThreads = kWaves * kWave;
 constexpr int kQW = 32;             // queries per wave
 constexpr int kQT = kWaves * kQW;   // queries per workgroup
 constexpr int kKT = 64;             // keys per tile
+constexpr int kSplitMaxQ = 64;      // sequences of at most this many queries take the split layout
 
 template <typename T, int HD>
 struct AttnCfg {
@@ -77,15 +82,20 @@ __device__ __forceinline__ int kswz(int r) {
     return r & 7;
 }
 
-template <typename T, int HD, bool kPacked>
+template <typename T, int HD, bool kPacked, bool kSplit>
 __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_scale_log2) {
   using C = AttnCfg<T, HD>;
+  static_assert(!(kPacked && kSplit), "the split layout serves unpacked sequences");
+  constexpr int NQB = kSplit ? 1 : 2;   // 16-query blocks per wave
+  constexpr int NH = kSplit ? 1 : 2;    // 32-key halves of a tile per wave
   __shared__ __attribute__((aligned(16))) uint8_t smem[2 * C::STAGE];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int fr = lane & 15, g = lane >> 4;
   const int b = blockIdx.z, h = blockIdx.y;
-  const int q0 = blockIdx.x * kQT + wave * kQW;
+  // split: the wave's query block and key half
+  const int qsel = kSplit ? (wave & 1) : 0, hsel = kSplit ? (wave >> 1) : 0;
+  const int q0 = kSplit ? int(blockIdx.x) * kQW + 16 * qsel : int(blockIdx.x) * kQT + wave * kQW;
   const size_t bh = size_t(b) * a.H + h;
 
   const T* Q = static_cast<const T*>(a.q) + bh * a.Sq * HD;
@@ -123,9 +133,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
   }
 
   // Q fragments (B operand of S^T = K Q^T): query q0 + 16 qb + fr, chunk 4 step + g
-  u32x4 qf[2][C::QSTEPS];
+  u32x4 qf[NQB][C::QSTEPS];
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
+  for (int qb = 0; qb < NQB; ++qb) {
     const int q = min(q0 + qb * 16 + fr, a.Sq - 1);
 #pragma unroll
     for (int st = 0; st < C::QSTEPS; ++st)
@@ -203,11 +213,17 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
     }
   };
 
-  f32x4 o[C::NDB][2];
+  f32x4 o[C::NDB][NQB];
 #pragma unroll
-  for (int db = 0; db < C::NDB; ++db) o[db][0] = o[db][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float mrun[2] = {-INFINITY, -INFINITY};   // running max of the scaled scores (exp2 domain)
-  float lrun[2] = {0.f, 0.f};
+  for (int db = 0; db < C::NDB; ++db)
+#pragma unroll
+    for (int qb = 0; qb < NQB; ++qb) o[db][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float mrun[NQB], lrun[NQB];   // exponent reference (log2 units) and this lane's part of the sum
+#pragma unroll
+  for (int qb = 0; qb < NQB; ++qb) {
+    mrun[qb] = -INFINITY;
+    lrun[qb] = 0.f;
+  }
 
   issue(0, 0);
   wait_vmcnt<0>();
@@ -231,26 +247,28 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
 
     // the tile's 64 keys in two halves of 32: S^T, online softmax and P V per half
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
+    for (int hh = 0; hh < NH; ++hh) {
+      const int half = kSplit ? hsel : hh;
       // S^T block (key block 2 half + kk, query block qb)
-      f32x4 sc[2][2];
+      f32x4 sc[2][NQB];
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
-        sc[kk][0] = sc[kk][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int qb = 0; qb < NQB; ++qb) sc[kk][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int st = 0; st < C::QSTEPS; ++st) {
           const int kr = key_of(half, kk, fr);
           const u32x4 kf = *reinterpret_cast<const u32x4*>(s + kr * (C::CK * 16) + (((4 * st + g) ^ kswz<T, C::CK>(kr)) << 4));
-          Mfma<T>::run(sc[kk][0], kf, qf[0][st]);
-          Mfma<T>::run(sc[kk][1], kf, qf[1][st]);
+#pragma unroll
+          for (int qb = 0; qb < NQB; ++qb) Mfma<T>::run(sc[kk][qb], kf, qf[qb][st]);
         }
       }
       // online softmax per query column (this lane's query q0 + 16 qb + fr)
-      float p[2][2][4];
-      float alpha[2];
+      float p[2][NQB][4];
+      float alpha[NQB];
       const bool full = !pmask && k0 + 32 * half + 32 <= nk;   // every key of this half is valid
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
+      for (int qb = 0; qb < NQB; ++qb) {
         float mt = -INFINITY;
         if (full) {   // wave-uniform: no key of this half is masked
 #pragma unroll
@@ -281,27 +299,32 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
         // reference so o / l is unchanged, and the accumulators are rescaled
         // rarely instead of at nearly every new maximum.
         const float mcand = mt * qk_scale_log2;
-        float mnew = mcand > mrun[qb] + 8.f ? mcand : mrun[qb];
-        // packed: a branch query can meet a tile whose keys it all masks
-        // before any key it sees; exponents then use 0 and give 0, not NaN
-        if constexpr (kPacked) mnew = mnew == -INFINITY ? 0.f : mnew;
-        alpha[qb] = __builtin_amdgcn_exp2f(mrun[qb] - mnew);
+        const float mnew = mcand > mrun[qb] + 8.f ? mcand : mrun[qb];
+        // packed (a branch query) or split (the second key half): a tile can
+        // mask every key a wave sees before it has seen any; the reference
+        // stays -inf and the exponents use 0, giving 0 instead of NaN
+        float mref = mnew;
+        if constexpr (kPacked || kSplit) mref = mnew == -INFINITY ? 0.f : mnew;
+        alpha[qb] = __builtin_amdgcn_exp2f(mrun[qb] - mref);
         mrun[qb] = mnew;
         float ls = 0.f;
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const float e = __builtin_amdgcn_exp2f(fmaf(p[kk][qb][i], qk_scale_log2, -mnew));
+            const float e = __builtin_amdgcn_exp2f(fmaf(p[kk][qb][i], qk_scale_log2, -mref));
             p[kk][qb][i] = e;
             ls += e;
           }
         lrun[qb] = lrun[qb] * alpha[qb] + ls;
       }
       // rescale the accumulators only when some query of the wave has a new maximum
-      if (__any(alpha[0] != 1.f || alpha[1] != 1.f)) {
+      bool moved = false;
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
+      for (int qb = 0; qb < NQB; ++qb) moved = moved || alpha[qb] != 1.f;
+      if (__any(moved)) {
+#pragma unroll
+        for (int qb = 0; qb < NQB; ++qb)
 #pragma unroll
           for (int db = 0; db < C::NDB; ++db) o[db][qb] *= alpha[qb];
       }
@@ -311,9 +334,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
         // lo = bf16(p - hi) (both rounded to nearest even), so the weights keep
         // about 16 significant bits: bf16 weights alone add an error as large as
         // the bf16 rounding of the output over a thousand keys.
-        u32x4 pb[2], pl[2];
+        u32x4 pb[NQB], pl[NQB];
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
+        for (int qb = 0; qb < NQB; ++qb)
 #pragma unroll
           for (int w = 0; w < 4; ++w) {
             const int kk = w >> 1, i0 = 2 * (w & 1);
@@ -327,7 +350,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
           // this lane's 8 probabilities are keys 32 half + 8 g .. + 7 (see key_of)
           const u32x4 vf = *reinterpret_cast<const u32x4*>(sv + swz(db * 16 + fr, 4 * half + g, C::CV * 16));
 #pragma unroll
-          for (int qb = 0; qb < 2; ++qb) {
+          for (int qb = 0; qb < NQB; ++qb) {
             Mfma<T>::run(o[db][qb], vf, pb[qb]);
             Mfma<T>::run(o[db][qb], vf, pl[qb]);
           }
@@ -335,9 +358,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
       } else {
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
-          u32x4 pb[2];
+          u32x4 pb[NQB];
 #pragma unroll
-          for (int qb = 0; qb < 2; ++qb)
+          for (int qb = 0; qb < NQB; ++qb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) pb[qb][i] = __float_as_uint(p[kk][qb][i]);
 #pragma unroll
@@ -345,8 +368,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
             const int r = db * 16 + fr;
             const int key = (2 * half + kk) * 16 + 4 * g;  // 4 fp32 keys = one chunk
             const u32x4 vf = *reinterpret_cast<const u32x4*>(sv + swz(r, key >> 2, C::CV * 16));
-            Mfma<T>::run(o[db][0], vf, pb[0]);
-            Mfma<T>::run(o[db][1], vf, pb[1]);
+#pragma unroll
+            for (int qb = 0; qb < NQB; ++qb) Mfma<T>::run(o[db][qb], vf, pb[qb]);
           }
         }
       }
@@ -359,9 +382,38 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
     }
   }
 
+  if constexpr (kSplit) {
+    // Merge the second key half's state into the first's, lane by lane (the
+    // same lane of the two waves holds the same query and dims): the ring is
+    // free after the loop's last barrier.  The first half always holds key 0,
+    // so its reference is finite; a second half that saw no key has l = 0
+    // and reference -inf, and weighs 0.
+    constexpr int NV = C::NDB * 4 + 2;
+    static_assert(2 * NV * 64 * 4 <= 2 * C::STAGE, "merge buffer inside the ring");
+    float* xs = reinterpret_cast<float*>(smem) + qsel * NV * 64 + lane;
+    if (hsel == 1) {
+#pragma unroll
+      for (int db = 0; db < C::NDB; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) xs[(4 * db + i) * 64] = o[db][0][i];
+      xs[(NV - 2) * 64] = mrun[0];
+      xs[(NV - 1) * 64] = lrun[0];
+    }
+    __syncthreads();
+    if (hsel == 1) return;
+    const float mb = xs[(NV - 2) * 64], lb = xs[(NV - 1) * 64];
+    const float m = fmaxf(mrun[0], mb);
+    const float sa = __builtin_amdgcn_exp2f(mrun[0] - m), sb = __builtin_amdgcn_exp2f(mb - m);
+#pragma unroll
+    for (int db = 0; db < C::NDB; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[db][0][i] = o[db][0][i] * sa + xs[(4 * db + i) * 64] * sb;
+    lrun[0] = lrun[0] * sa + lb * sb;
+  }
+
   // normalise and store O[b * Sq + q][h * HD + dim]
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
+  for (int qb = 0; qb < NQB; ++qb) {
     const float l = group4_sum(lrun[qb]);
     const float inv = 1.0f / l;
     const int q = q0 + qb * 16 + fr;
@@ -383,9 +435,14 @@ hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
     return hipErrorInvalidValue;
   const float scale = 1.4426950408889634f / sqrtf(float(HD));
   if (a.pack_B > 0)
-    hipLaunchKernelGGL((attn_kernel<T, HD, true>), dim3(cdiv(a.Sq, kQT), a.H, a.B), dim3(kThreads), 0, s, a, scale);
+    hipLaunchKernelGGL((attn_kernel<T, HD, true, false>), dim3(cdiv(a.Sq, kQT), a.H, a.B), dim3(kThreads), 0, s, a,
+                       scale);
+  else if (a.Sq <= kSplitMaxQ)
+    hipLaunchKernelGGL((attn_kernel<T, HD, false, true>), dim3(cdiv(a.Sq, kQW), a.H, a.B), dim3(kThreads), 0, s, a,
+                       scale);
   else
-    hipLaunchKernelGGL((attn_kernel<T, HD, false>), dim3(cdiv(a.Sq, kQT), a.H, a.B), dim3(kThreads), 0, s, a, scale);
+    hipLaunchKernelGGL((attn_kernel<T, HD, false, false>), dim3(cdiv(a.Sq, kQT), a.H, a.B), dim3(kThreads), 0, s, a,
+                       scale);
   return hipGetLastError();
 }
 
