@@ -223,6 +223,36 @@ def test_cached_prefix_forward_tiny(P, tiny):
     print(compare_stats(out.numpy(), ref, 1e-4, label="cached forward"))
 
 
+@pytest.mark.parametrize("Pn,Bk", [(20, 1), (20, 32), (100, 17), (130, 64), (64, 33)])
+def test_cached_prefix_forward_small_bf16(P, small_bf16, Pn, Bk):
+    """Blocks of at most 64 queries over a cached bf16 prefix (the attention
+    layout that splits a tile's keys between two waves and merges their
+    softmax states): a prefix shorter than half a key tile, ragged prefix
+    tiles, single-query blocks, against the mirror oracle."""
+    shape, w_np, model = small_bf16
+    nb = 3
+    prefix = synth.tokens_np(40 + Pn, "prefix", Pn, shape.vocab - 1)
+    k, vt, cap = model.new_kv_cache(Pn)
+    from paper_2608_11742_amd._abi import KvCache
+    kvc = KvCache(k.data_ptr(), vt.data_ptr(), 0, cap)
+    model.forward(torch.from_numpy(prefix).to(DEV)[None], torch.arange(1, dtype=torch.int32, device=DEV),
+                  kv_out=kvc)
+    blocks = synth.tokens_np(41 + Bk, "blocks", nb * Bk, shape.vocab).reshape(nb, Bk)
+    blocks[:, Bk // 3:] = shape.mask_id
+    lm = np.arange(Bk, dtype=np.int32)
+    kvc.len = Pn
+    out = model.forward(torch.from_numpy(blocks).to(DEV), torch.from_numpy(lm).to(DEV), pos_offset=Pn,
+                        kv_prefix=kvc, scale=3.0)
+    torch.cuda.synchronize()
+    kv = om.prefix_cache(prefix, w_np, shape, mirror=True)
+    refs = []
+    for b in range(nb):
+        h = om.hidden(blocks[b], w_np, shape, pos_offset=Pn, mirror=True, prefix_kv=kv)
+        refs.append(om.lm_logits(h, w_np, shape, scale=3.0))
+    ref = softmax_stats(np.concatenate(refs), 16)
+    print(compare_stats(out.numpy(), ref, 2e-2, margin="auto", label=f"cached bf16 prefix {Pn} block {Bk}"))
+
+
 def test_probe_logits(P, tiny):
     shape, w_np, model = tiny
     S = 64
