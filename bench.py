@@ -143,23 +143,12 @@ def timed(fn, n):
     return (time.perf_counter() - t0) / n
 
 
-def other_configs(P, model, shape, n):
-    """The other 8B-shape configurations, on the same weights."""
+def cached_step(P, model, shape, n):
+    """KV-cached RPS step: 1024 cached prefix positions, 16 branch blocks of 32."""
     from paper_2608_11742_amd._abi import KvCache
     dev = torch.device("cuda:0")
     out = {}
     weights_gb = 2.0 * shape.n_params() / 1e9
-
-    # single denoising forward, 1 x 512, statistics on the 256 masked rows
-    wl = W.WORKLOADS["b8_forward_bf16"]
-    tokens, m_pos, base = build_state(P, model, wl, dev)
-    t = timed(lambda: model.forward(tokens[None], m_pos, out=base), n)
-    fl = step_flops(shape, 1, wl.seq, wl.gen_len)
-    out[wl.name] = {"forwards_per_s": round(1.0 / t, 2), "ms": round(t * 1e3, 3),
-                    "tflops": round(fl / t / 1e12, 1), "tflop": round(fl / 1e12, 2)}
-    log(f"{wl.name}: {t * 1e3:.2f} ms")
-
-    # KV-cached RPS step: 1024 cached prefix positions, 16 branch blocks of 32
     wl = W.WORKLOADS["b8_cached_step_bf16"]
     prefix = synth.tokens_torch(W.SEED_PROMPT, "prefix", wl.prompt_len, shape.vocab - 1, device=dev)
     k, vt, cap = model.new_kv_cache(wl.prompt_len)
@@ -193,6 +182,24 @@ def other_configs(P, model, shape, n):
                     "gbs": round((weights_gb + kv_gb) / t, 1),
                     "algorithmic_gb": round(weights_gb + kv_gb, 2), "tflop": round(fl / 1e12, 2)}
     log(f"{wl.name}: {t * 1e3:.2f} ms")
+    return out
+
+
+def other_configs(P, model, shape, n):
+    """The other 8B-shape configurations, on the same weights."""
+    dev = torch.device("cuda:0")
+    out = {}
+
+    # single denoising forward, 1 x 512, statistics on the 256 masked rows
+    wl = W.WORKLOADS["b8_forward_bf16"]
+    tokens, m_pos, base = build_state(P, model, wl, dev)
+    t = timed(lambda: model.forward(tokens[None], m_pos, out=base), n)
+    fl = step_flops(shape, 1, wl.seq, wl.gen_len)
+    out[wl.name] = {"forwards_per_s": round(1.0 / t, 2), "ms": round(t * 1e3, 3),
+                    "tflops": round(fl / t / 1e12, 1), "tflop": round(fl / 1e12, 2)}
+    log(f"{wl.name}: {t * 1e3:.2f} ms")
+
+    out.update(cached_step(P, model, shape, n))
 
     # full blockwise decode of 256 tokens (Algorithm 1)
     wl = W.WORKLOADS["b8_decode_bf16"]
@@ -269,6 +276,8 @@ def main():
     ap.add_argument("--layers", type=int, default=0, help="override layer count (profiling runs only)")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the other 8B configurations (single forward, cached step, full decode)")
+    ap.add_argument("--cached-only", action="store_true",
+                    help="only run the KV-cached RPS step --steps times and print its figures (profiling runs)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain copy of MIB mebibytes (scale for rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -297,6 +306,10 @@ def main():
         f"({shape.n_params() / 1e9:.2f} B params)")
     max_pos = max(x.seq for x in W.WORKLOADS.values() if x.model == W.WORKLOADS["b8_rps_step_bf16"].model)
     model = P.Model(shape, w, dtype="bf16", max_pos=max_pos)
+    if args.cached_only:
+        print(json.dumps(cached_step(P, model, shape, args.steps)), flush=True)
+        model.close()
+        return
     tokens, m_pos, base = build_state(P, model, wl, dev)
     prm = P.params(mode=wl.pivot_mode, k_max=wl.k_max, tau_pivot=wl.tau_pivot, pct_lo=wl.pct_lo,
                    pct_hi=wl.pct_hi, n_pivots=wl.n_pivots, r=wl.r, n_cand=wl.n_cand, max_branch=wl.capacity)

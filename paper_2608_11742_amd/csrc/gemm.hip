@@ -117,6 +117,34 @@ __device__ __forceinline__ int qkv_pos(const QkvOut& o, int row) {
   return o.pos_offset + (o.pack_B && r >= o.pack_S ? o.pack_b0 + ((r - o.pack_S) & (o.pack_B - 1)) : r);
 }
 
+// Tile and K part of a split-K workgroup (grid: tiles x parts).  Workgroups
+// are dispatched to the 8 XCDs round-robin by linear id; when the part count
+// divides 8 or is a multiple of 8, each XCD gets whole parts (or an even share
+// of one part's tiles, the row tiles of a column tile together), so that all
+// readers of an A or B panel of a part share one L2 and the panel is fetched
+// once, instead of once per XCD.  The part a workgroup computes, and so the
+// summation order, does not depend on this mapping.
+__device__ __forceinline__ void map_split_tile(int tiles_m, int tiles_n, int parts, int& tm, int& tn, int& part) {
+  const int T = tiles_m * tiles_n;
+  const int L = int(blockIdx.x) + int(gridDim.x) * int(blockIdx.y);
+  const int xcd = L % 8, local = L / 8;
+  int j;
+  if (parts % 8 == 0) {
+    part = xcd * (parts / 8) + local / T;
+    j = local % T;
+  } else if (8 % parts == 0 && T % (8 / parts) == 0) {
+    const int per = 8 / parts;   // XCDs per part
+    part = xcd / per;
+    j = (xcd % per) * (T / per) + local;
+  } else {
+    part = blockIdx.y;
+    map_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, kGroupM, tm, tn);
+    return;
+  }
+  tm = j % tiles_m;
+  tn = j / tiles_m;
+}
+
 // HD: head_dim of the QKV epilogue (compile-time, so the rotary partner block
 // index stays static and the accumulators stay in registers); 0 otherwise.
 template <typename T, int EPI, int HD, class Cfg>
@@ -128,17 +156,20 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
   using TM = TileMma<T, Cfg::BM, Cfg::BN, Cfg::WM, Cfg::WN, kTrans>;
   constexpr bool kSplit = EPI == EPI_PART || EPI == EPI_PART_GU;
   __shared__ __attribute__((aligned(16))) uint8_t smem[TM::kSmem];
-  int tm, tn;
-  map_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, kGroupM, tm, tn);
+  int tm, tn, part = 0;
+  if constexpr (kSplit)
+    map_split_tile(tiles_m, tiles_n, gridDim.y, tm, tn, part);
+  else
+    map_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, kGroupM, tm, tn);
   const int m0 = tm * kBM;
   const uint32_t a_row_bytes = uint32_t(lda) * sizeof(T);
   const uint32_t b_row_bytes = uint32_t(ldb) * sizeof(T);
   // K stages of this part (128 bytes of every row per stage)
   int st0 = 0, nst = K / (2 * TM::kKPerStage);
   if constexpr (kSplit) {
-    const int all = nst, split = blockIdx.y;
-    st0 = split * all / int(gridDim.y);
-    nst = (split + 1) * all / int(gridDim.y) - st0;
+    const int all = nst;
+    st0 = part * all / int(gridDim.y);
+    nst = (part + 1) * all / int(gridDim.y) - st0;
   }
   const uint32_t k_bytes = uint32_t(st0) * TM::kRowBytes;
   auto a_off = [&](int r) -> uint32_t { return uint32_t(min(m0 + r, M - 1)) * a_row_bytes + k_bytes; };
@@ -166,7 +197,7 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
     static_assert(TM::kWTM % 64 == 0 && TM::kWTN == 128, "partial epilogue tiling");
     uint8_t* st = smem + wave * (64 * 64 * 4);
     auto slot_of = [](int r, int c4) { return r * 256 + (((c4 ^ (r & 15))) << 4); };
-    float* P = ep.part + size_t(blockIdx.y) * M * ep.np;
+    float* P = ep.part + size_t(part) * M * ep.np;
 #pragma unroll
     for (int g = 0; g < TM::kWTM / 64; ++g) {   // 64-row groups of the wave tile
       const int r0 = m0 + wm * TM::kWTM + 64 * g;
