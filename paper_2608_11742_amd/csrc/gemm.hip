@@ -471,12 +471,12 @@ __global__ __launch_bounds__(kRedThreads) void splitk_resid_kernel(const float* 
   f32x4 acc = *reinterpret_cast<const f32x4*>(x + size_t(row) * ldx + c);
   auto pr = [&](int p) { return *reinterpret_cast<const f32x4*>(part + (size_t(p) * M + row) * np + c); };
   int p = 0;
-  for (; p + 4 <= splits; p += 4) {   // four loads in flight, added in order
-    const f32x4 a0 = pr(p), a1 = pr(p + 1), a2 = pr(p + 2), a3 = pr(p + 3);
-    acc += a0;
-    acc += a1;
-    acc += a2;
-    acc += a3;
+  for (; p + 8 <= splits; p += 8) {   // eight loads in flight, added in order
+    f32x4 a[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) a[q] = pr(p + q);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc += a[q];
   }
   for (; p < splits; ++p) acc += pr(p);
   *reinterpret_cast<f32x4*>(x + size_t(row) * ldx + c) = acc;
@@ -603,7 +603,13 @@ int gemm_splits(int M, int tiles_n, int K, int dtype) {
   const int tiles = cdiv(M, small ? Small::BM : Big::BM) * tiles_n, full = small ? 512 : 256;
   const int stages = K / (dtype ? 64 : 32);   // 128-byte K stages
   if (tiles >= full * 5 / 8 || stages < 2) return 1;
-  return std::max(1, std::min(full / tiles, stages / 4));
+  const int parts = std::max(1, std::min(full / tiles, stages / 4));
+  // a multiple of 8 or a power of two, so that map_split_tile gives each
+  // XCD whole parts (or an even share of one)
+  if (parts >= 8) return parts / 8 * 8;
+  int p2 = 1;
+  while (p2 * 2 <= parts) p2 *= 2;
+  return p2;
 }
 
 size_t gemm_partial_bytes(int M, int tiles_n, int splits) {

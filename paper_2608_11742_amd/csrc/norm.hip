@@ -28,6 +28,7 @@ __device__ __forceinline__ void store4(bf16_t* p, f32x4 v) {
 __device__ __forceinline__ void store4(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
 
 constexpr int kNormChunks = 8;   // 16-byte chunks per thread held in registers: d <= 8192
+constexpr int kFewRows = 256;    // fewer rows than CUs: resid_rmsnorm adds the partials column-parallel
 
 // One workgroup per output row; the row stays in registers between the sum
 // of squares (reduced in fp32 over 4 waves) and the scaled store.
@@ -148,6 +149,16 @@ hipError_t rmsnorm(int dtype, const float* x, int d, float eps, int rows, const 
 hipError_t resid_rmsnorm(int dtype, const float* part, int splits, int np, int M, float* x, int d, float eps,
                          void* out, hipStream_t s) {
   if (d % 4 || np % 4 || d > kNormChunks * kRowThreads * 4) return hipErrorInvalidValue;
+  if (M < kFewRows) {
+    // One workgroup per row would leave most CUs idle while each walks every
+    // partial of its row: add the partials column-parallel (same order), then
+    // normalise.
+    if (np != cdiv(d, 256) * 256) return hipErrorInvalidValue;   // the pitch splitk_add assumes
+    const SplitK sk{const_cast<float*>(part), splits, true};
+    const hipError_t e = splitk_add(sk, M, d, x, d, s);
+    if (e != hipSuccess) return e;
+    return rmsnorm(dtype, x, d, eps, M, nullptr, 1, 1, out, s);
+  }
   if (dtype)
     hipLaunchKernelGGL(resid_rmsnorm_kernel<bf16_t>, dim3(M), dim3(kRowThreads), 0, s, part, splits, np, M, x, d, eps,
                        static_cast<bf16_t*>(out));
