@@ -4,10 +4,11 @@
 //
 // A workgroup of 4 waves takes 128 queries of one (sequence, head); each
 // wave owns 32 queries, two workgroups share a CU.  Short sequences (at most
-// 64 queries, e.g. a block recomputed over a cached prefix) take 32 queries
-// per workgroup instead: wave w owns the 16 queries of block w % 2 and the
-// keys of half w / 2 of every tile, and the two halves' softmax states are
-// merged at the end, so no wave computes clamped duplicate queries.  Keys stream through a
+// 64 queries, e.g. a block recomputed over a cached prefix), and launches
+// whose 128-query workgroups would leave CUs idle (a single sequence of
+// 512), take 32 queries per workgroup instead: wave w owns the 16 queries of
+// block w % 2 and the keys of half w / 2 of every tile, and the two halves'
+// softmax states are merged at the end.  Keys stream through a
 // two-slot LDS ring in tiles of 64 (K rows and V^T columns), copied from
 // global memory straight into LDS with buffer_load ... lds one tile ahead.
 // Scores are computed transposed, S^T = K Q^T, so in the MFMA output layout
@@ -29,6 +30,7 @@ constexpr int kQW = 32;             // queries per wave
 constexpr int kQT = kWaves * kQW;   // queries per workgroup
 constexpr int kKT = 64;             // keys per tile
 constexpr int kSplitMaxQ = 64;      // sequences of at most this many queries take the split layout
+constexpr int kSplitMaxWg = 256;    // so do launches whose 128-query layout has fewer workgroups than this
 
 template <typename T, int HD>
 struct AttnCfg {
@@ -437,7 +439,7 @@ hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
   if (a.pack_B > 0)
     hipLaunchKernelGGL((attn_kernel<T, HD, true, false>), dim3(cdiv(a.Sq, kQT), a.H, a.B), dim3(kThreads), 0, s, a,
                        scale);
-  else if (a.Sq <= kSplitMaxQ)
+  else if (a.Sq <= kSplitMaxQ || cdiv(a.Sq, kQT) * a.H * a.B < kSplitMaxWg)
     hipLaunchKernelGGL((attn_kernel<T, HD, false, true>), dim3(cdiv(a.Sq, kQW), a.H, a.B), dim3(kThreads), 0, s, a,
                        scale);
   else

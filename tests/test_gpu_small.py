@@ -90,9 +90,9 @@ def test_vocab_entropy_topk_is_deterministic_and_ignores_workspace_contents(P):
 
 # ------------------------------------------------------------ dllm_forward
 
-def test_forward_tiny_f32_ragged_batch(P, tiny):
+@pytest.mark.parametrize("B_,S", [(3, 50), (1, 130)])
+def test_forward_tiny_f32_ragged_batch(P, tiny, B_, S):
     shape, w_np, model = tiny
-    B_, S = 3, 50
     toks = synth.tokens_np(3, "toks", B_ * S, shape.vocab).reshape(B_, S)
     toks[:, 30:] = shape.mask_id
     lm_pos = np.array([0, 7, 29, 30, 31, 40, 45, 49], dtype=np.int32)
@@ -180,10 +180,12 @@ def test_forward_small_bf16_many_sequences(P, small_bf16):
                             label=f"64 x 200 bf16 seq {b}"))
 
 
-@pytest.mark.parametrize("S", [40, 64])
+@pytest.mark.parametrize("S", [40, 64, 150])
 def test_forward_small_bf16_few_rows(P, small_bf16, S):
     """Few-row forwards (the 64-row GEMM tiles and split-K reductions of a
-    block forward) against the mirror oracle."""
+    block forward; at 150 rows, attention in the 32-query layout that a
+    launch with fewer 128-query workgroups than CUs takes) against the
+    mirror oracle."""
     shape, w_np, model = small_bf16
     toks = synth.tokens_np(15 + S, "toks", S, shape.vocab - 1)
     toks[S // 2:] = shape.mask_id
