@@ -518,11 +518,11 @@ __global__ __launch_bounds__(kRedThreads) void splitk_swiglu_kernel(const float*
 // Q and K: one thread per (row, q or k, head, dim < HD/2) pair; sums the two
 // partners, rotates them and writes both to the head-major layout
 template <typename T, int HD>
-__global__ __launch_bounds__(kRedThreads) void splitk_qk_kernel(const float* __restrict__ part, int splits, int M,
-                                                                int np, QkvOut o) {
+__device__ __forceinline__ void splitk_qk(const float* __restrict__ part, int splits, int M, int np,
+                                          const QkvOut& o, int blk) {
   constexpr int half = HD / 2;
   const int d = o.d;
-  const int i = blockIdx.x * kRedThreads + threadIdx.x;
+  const int i = blk * kRedThreads + threadIdx.x;
   if (i >= M * d) return;
   const int row = i / d, p = i - row * d;
   const int which = p / (d / 2), rest = p - which * (d / 2);
@@ -554,10 +554,9 @@ __global__ __launch_bounds__(kRedThreads) void splitk_qk_kernel(const float* __r
 // V: 16-row x 64-column tiles transposed through LDS so that both the partial
 // reads (along columns) and the V^T writes (along positions) are contiguous
 template <typename T>
-__global__ __launch_bounds__(kRedThreads) void splitk_v_kernel(const float* __restrict__ part, int splits, int M,
-                                                               int np, QkvOut o) {
-  __shared__ float tile[16][65];
-  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 16, d = o.d;
+__device__ __forceinline__ void splitk_v(const float* __restrict__ part, int splits, int M, int np, const QkvOut& o,
+                                         int bx, int by, float (&tile)[16][65]) {
+  const int c0 = bx * 64, r0 = by * 16, d = o.d;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const int idx = threadIdx.x + kRedThreads * e, r = idx >> 6, c = idx & 63, row = r0 + r, col = c0 + c;
@@ -585,6 +584,21 @@ __global__ __launch_bounds__(kRedThreads) void splitk_v_kernel(const float* __re
     if (row >= M || col >= d) continue;
     const int b = row / o.seq, sp = row - b * o.seq, h = col / o.hd, dim = col - h * o.hd;
     store_f(static_cast<T*>(o.vt) + (size_t(b * o.H + h) * o.hd + dim) * o.vt_ld + sp, tile[r][c]);
+  }
+}
+
+// the QKV split-K sums in one launch: blocks 0 .. n_qk - 1 take Q and K, the
+// rest the V tiles (d / 64 column tiles by M / 16 row tiles)
+template <typename T, int HD>
+__global__ __launch_bounds__(kRedThreads) void splitk_qkv_kernel(const float* __restrict__ part, int splits, int M,
+                                                                 int np, QkvOut o, int n_qk) {
+  __shared__ float tile[16][65];
+  const int blk = blockIdx.x;
+  if (blk < n_qk) {
+    splitk_qk<T, HD>(part, splits, M, np, o, blk);
+  } else {
+    const int v = blk - n_qk, nvx = cdiv(o.d, 64);
+    splitk_v<T>(part, splits, M, np, o, v % nvx, v / nvx, tile);
   }
 }
 
@@ -693,13 +707,13 @@ hipError_t qkv_split(const void* A, int lda, const void* Wqkv, int M, int K, con
   ep.np = tn * kBN;
   hipError_t e = launch<T, EPI_PART>(A, lda, Wqkv, K, M, N, K, tn, ep, s, sk.splits);
   if (e != hipSuccess) return e;
-  const dim3 g(cdiv(M * o.d, kRedThreads));
+  const int n_qk = cdiv(M * o.d, kRedThreads), n_v = cdiv(o.d, 64) * cdiv(M, 16);
   if (o.hd == 128)
-    hipLaunchKernelGGL((splitk_qk_kernel<T, 128>), g, dim3(kRedThreads), 0, s, sk.part, sk.splits, M, ep.np, o);
+    hipLaunchKernelGGL((splitk_qkv_kernel<T, 128>), dim3(n_qk + n_v), dim3(kRedThreads), 0, s, sk.part, sk.splits,
+                       M, ep.np, o, n_qk);
   else
-    hipLaunchKernelGGL((splitk_qk_kernel<T, 64>), g, dim3(kRedThreads), 0, s, sk.part, sk.splits, M, ep.np, o);
-  hipLaunchKernelGGL(splitk_v_kernel<T>, dim3(cdiv(o.d, 64), cdiv(M, 16)), dim3(kRedThreads), 0, s, sk.part,
-                     sk.splits, M, ep.np, o);
+    hipLaunchKernelGGL((splitk_qkv_kernel<T, 64>), dim3(n_qk + n_v), dim3(kRedThreads), 0, s, sk.part, sk.splits,
+                       M, ep.np, o, n_qk);
   return hipGetLastError();
 }
 

@@ -28,7 +28,8 @@ __device__ __forceinline__ void store4(bf16_t* p, f32x4 v) {
 __device__ __forceinline__ void store4(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
 
 constexpr int kNormChunks = 8;   // 16-byte chunks per thread held in registers: d <= 8192
-constexpr int kFewRows = 256;    // fewer rows than CUs: resid_rmsnorm adds the partials column-parallel
+constexpr int kFewRows = 256;    // fewer rows than CUs: resid_rmsnorm takes kWideThreads per row
+constexpr int kWideThreads = 1024;
 
 // One workgroup per output row; the row stays in registers between the sum
 // of squares (reduced in fp32 over 4 waves) and the scaled store.
@@ -66,29 +67,31 @@ __global__ __launch_bounds__(kRowThreads) void rmsnorm_kernel(const float* __res
 // Residual update from split-K partial tiles fused with the RMSNorm that
 // follows it: x[r] += part[0][r] + part[1][r] + ... (in this order, as the
 // separate reduction), then out[r] = x[r] / sqrt(mean(x[r]^2) + eps).
-template <typename T>
-__global__ __launch_bounds__(kRowThreads) void resid_rmsnorm_kernel(const float* __restrict__ part, int splits,
-                                                                    int np, int M, float* __restrict__ x, int d,
-                                                                    float eps, T* __restrict__ out) {
-  __shared__ float red[kRowThreads / kWave];
+template <typename T, int THREADS>
+__global__ __launch_bounds__(THREADS) void resid_rmsnorm_kernel(const float* __restrict__ part, int splits, int np,
+                                                                int M, float* __restrict__ x, int d, float eps,
+                                                                T* __restrict__ out) {
+  constexpr int CH = kNormChunks * kRowThreads / THREADS;   // 16-byte chunks per thread: d <= 8192
+  constexpr int LIF = CH <= 2 ? 8 : 4;                       // partial loads in flight per chunk
+  __shared__ float red[THREADS / kWave];
   const int r = blockIdx.x;
   float* xr = x + size_t(r) * d;
   auto pr = [&](int p, int c) { return *reinterpret_cast<const f32x4*>(part + (size_t(p) * M + r) * np + c); };
-  f32x4 v[kNormChunks];
+  f32x4 v[CH];
   float ss = 0.f;
 #pragma unroll
-  for (int j = 0; j < kNormChunks; ++j) {
-    const int c = (threadIdx.x + j * kRowThreads) * 4;
+  for (int j = 0; j < CH; ++j) {
+    const int c = (threadIdx.x + j * THREADS) * 4;
     v[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     if (c < d) {
       v[j] = *reinterpret_cast<const f32x4*>(xr + c);
       int p = 0;
-      for (; p + 4 <= splits; p += 4) {   // four loads in flight, added in order
-        const f32x4 a0 = pr(p, c), a1 = pr(p + 1, c), a2 = pr(p + 2, c), a3 = pr(p + 3, c);
-        v[j] += a0;
-        v[j] += a1;
-        v[j] += a2;
-        v[j] += a3;
+      for (; p + LIF <= splits; p += LIF) {   // LIF loads in flight, added in order
+        f32x4 a[LIF];
+#pragma unroll
+        for (int q = 0; q < LIF; ++q) a[q] = pr(p + q, c);
+#pragma unroll
+        for (int q = 0; q < LIF; ++q) v[j] += a[q];
       }
       for (; p < splits; ++p) v[j] += pr(p, c);
       *reinterpret_cast<f32x4*>(xr + c) = v[j];
@@ -100,12 +103,12 @@ __global__ __launch_bounds__(kRowThreads) void resid_rmsnorm_kernel(const float*
   __syncthreads();
   float tot = 0.f;
 #pragma unroll
-  for (int w = 0; w < kRowThreads / kWave; ++w) tot += red[w];
+  for (int w = 0; w < THREADS / kWave; ++w) tot += red[w];
   const float inv = 1.0f / sqrtf(tot / float(d) + eps);
   T* o = out + size_t(r) * d;
 #pragma unroll
-  for (int j = 0; j < kNormChunks; ++j) {
-    const int c = (threadIdx.x + j * kRowThreads) * 4;
+  for (int j = 0; j < CH; ++j) {
+    const int c = (threadIdx.x + j * THREADS) * 4;
     if (c < d) store4(o + c, v[j] * inv);
   }
 }
@@ -149,22 +152,24 @@ hipError_t rmsnorm(int dtype, const float* x, int d, float eps, int rows, const 
 hipError_t resid_rmsnorm(int dtype, const float* part, int splits, int np, int M, float* x, int d, float eps,
                          void* out, hipStream_t s) {
   if (d % 4 || np % 4 || d > kNormChunks * kRowThreads * 4) return hipErrorInvalidValue;
-  if (M < kFewRows) {
-    // One workgroup per row would leave most CUs idle while each walks every
-    // partial of its row: add the partials column-parallel (same order), then
-    // normalise.
-    if (np != cdiv(d, 256) * 256) return hipErrorInvalidValue;   // the pitch splitk_add assumes
-    const SplitK sk{const_cast<float*>(part), splits, true};
-    const hipError_t e = splitk_add(sk, M, d, x, d, s);
-    if (e != hipSuccess) return e;
-    return rmsnorm(dtype, x, d, eps, M, nullptr, 1, 1, out, s);
+  // Fewer rows than CUs: 1024 threads per row, so that each thread walks the
+  // partials of fewer columns with more loads in flight.
+  const bool wide = M < kFewRows;
+  if (dtype) {
+    if (wide)
+      hipLaunchKernelGGL((resid_rmsnorm_kernel<bf16_t, kWideThreads>), dim3(M), dim3(kWideThreads), 0, s, part,
+                         splits, np, M, x, d, eps, static_cast<bf16_t*>(out));
+    else
+      hipLaunchKernelGGL((resid_rmsnorm_kernel<bf16_t, kRowThreads>), dim3(M), dim3(kRowThreads), 0, s, part,
+                         splits, np, M, x, d, eps, static_cast<bf16_t*>(out));
+  } else {
+    if (wide)
+      hipLaunchKernelGGL((resid_rmsnorm_kernel<float, kWideThreads>), dim3(M), dim3(kWideThreads), 0, s, part,
+                         splits, np, M, x, d, eps, static_cast<float*>(out));
+    else
+      hipLaunchKernelGGL((resid_rmsnorm_kernel<float, kRowThreads>), dim3(M), dim3(kRowThreads), 0, s, part,
+                         splits, np, M, x, d, eps, static_cast<float*>(out));
   }
-  if (dtype)
-    hipLaunchKernelGGL(resid_rmsnorm_kernel<bf16_t>, dim3(M), dim3(kRowThreads), 0, s, part, splits, np, M, x, d, eps,
-                       static_cast<bf16_t*>(out));
-  else
-    hipLaunchKernelGGL(resid_rmsnorm_kernel<float>, dim3(M), dim3(kRowThreads), 0, s, part, splits, np, M, x, d, eps,
-                       static_cast<float*>(out));
   return hipGetLastError();
 }
 
