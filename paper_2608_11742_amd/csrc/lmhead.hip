@@ -437,7 +437,10 @@ __global__ __launch_bounds__(256) void probe_kernel(const T* __restrict__ Hs, co
 
 int slices_for(int R, int V) {
   const int rt = cdiv(R, tile_rows(R)), vt = cdiv(V, kCols);
-  return std::max(1, std::min(vt, cdiv(kTargetWg, rt)));
+  // one row tile (a block of at most 128 rows): one workgroup per CU, so the
+  // merge folds half as many partials per row as with two rounds of slices
+  const int target = rt == 1 ? kTargetWg / 2 : kTargetWg;
+  return std::max(1, std::min(vt, cdiv(target, rt)));
 }
 
 int partials_per_row(int R, int V) { return slices_for(R, V) * (kThreads / tile_rows(R)); }
