@@ -232,6 +232,11 @@ typedef enum {
     DLLM_PROF_LMHEAD_MERGE = 8, DLLM_PROF_OTHER = 9
 } dllm_prof_class;
 dllm_status dllm_profile_begin(dllm_model* m, int32_t max_launches);
+/* As dllm_profile_begin, bracketing only the launches of the classes whose
+ * bit (1 << class) is set in class_mask: each pair of events costs a few
+ * microseconds of stream time, so a benchmark that times whole steps
+ * brackets only the kernel it reports on.  class_mask == 0 is EINVAL. */
+dllm_status dllm_profile_begin_classes(dllm_model* m, int32_t max_launches, uint32_t class_mask);
 dllm_status dllm_profile_end(dllm_model* m, float* ms, int32_t* launches);
 
 /* ---------------------------------------------------------------- scheduler */

@@ -134,8 +134,15 @@ def dllm_model_destroy(handle):
     lib().dllm_model_destroy(handle)
 
 
-def dllm_profile_begin(handle, max_launches: int = 20000):
-    _check(lib().dllm_profile_begin(handle, max_launches))
+def dllm_profile_begin(handle, max_launches: int = 20000, classes=None):
+    """classes: optional iterable of kernel-class names (PROF_NAMES) to bracket; default all."""
+    if classes is None:
+        _check(lib().dllm_profile_begin(handle, max_launches))
+        return
+    mask = 0
+    for name in classes:
+        mask |= 1 << _abi.PROF_NAMES.index(name)
+    _check(lib().dllm_profile_begin_classes(handle, max_launches, mask))
 
 
 def dllm_profile_end(handle) -> dict:

@@ -25,6 +25,7 @@ struct dllm_model {
   std::vector<int> prof_cls;
   int prof_used = 0;
   bool prof_on = false;
+  uint32_t prof_mask = ~0u;   // classes bracketed while profiling
 };
 
 namespace {
@@ -35,7 +36,7 @@ struct ProfScope {
   hipStream_t s;
   int idx = -1;
   ProfScope(dllm_model* m_, hipStream_t s_, int cls) : m(m_), s(s_) {
-    if (!m->prof_on || m->prof_used >= int(m->prof_cls.size())) return;
+    if (!m->prof_on || !((m->prof_mask >> cls) & 1u) || m->prof_used >= int(m->prof_cls.size())) return;
     idx = m->prof_used++;
     m->prof_cls[idx] = cls;
     (void)hipEventRecord(m->prof_ev[2 * idx], s);
@@ -224,7 +225,13 @@ void dllm_model_destroy(dllm_model* m) {
 }
 
 dllm_status dllm_profile_begin(dllm_model* m, int32_t max_launches) {
+  return dllm_profile_begin_classes(m, max_launches, ~0u);
+}
+
+dllm_status dllm_profile_begin_classes(dllm_model* m, int32_t max_launches, uint32_t class_mask) {
   if (!m || max_launches < 1) return fail(DLLM_EINVAL, "dllm_profile_begin: NULL model or max_launches < 1");
+  if (class_mask == 0) return fail(DLLM_EINVAL, "dllm_profile_begin_classes: empty class mask");
+  m->prof_mask = class_mask;
   const size_t need = size_t(2) * max_launches;
   while (m->prof_ev.size() < need) {
     hipEvent_t e;
