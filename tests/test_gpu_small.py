@@ -468,3 +468,20 @@ def test_tiny_rps_step_matches_oracle(P, tiny):
         assert stp.n_m == len(state.m_pos)
         assert np.array_equal(stp.m_pos.cpu().numpy()[:stp.n_m], state.m_pos)
         assert np.max(np.abs(stp.base.H.cpu().numpy()[:stp.n_m] - state.stats.H)) < 1e-4
+
+
+def test_profile_begin_classes_brackets_only_the_chosen_classes(P, tiny):
+    """Class-selective kernel timing (the benchmark brackets only the launch
+    it reports on): one forward bracketed for attention only counts exactly
+    the attention launches; an empty class mask is rejected."""
+    from paper_2608_11742_amd import binding as Bd
+    shape, w_np, model = tiny
+    toks = torch.from_numpy(synth.tokens_np(5, "toks", 2 * 40, shape.vocab).reshape(2, 40)).to(DEV)
+    lm_pos = torch.arange(8, dtype=torch.int32, device=DEV)
+    P.dllm_profile_begin(model.handle, 1000, classes=["attention"])
+    model.forward(toks, lm_pos)
+    prof = P.dllm_profile_end(model.handle)
+    assert prof["attention"][1] == shape.n_layers and prof["attention"][0] > 0
+    assert all(n == 0 for name, (_, n) in prof.items() if name != "attention")
+    with pytest.raises(Bd.DllmError):
+        Bd._check(Bd.lib().dllm_profile_begin_classes(model.handle, 10, 0))
