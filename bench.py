@@ -283,7 +283,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the lookahead branches would shard "
-              "across GPUs by data parallelism, which this build does not implement.", file=sys.stderr)
+              "across GPUs by data parallelism, which this implementation does not provide.", file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
