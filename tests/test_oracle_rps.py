@@ -30,12 +30,34 @@ def planted(rows):
 
 # ------------------------------------------------------------ standard commit
 
+def dyadic(rows, k=16):
+    """Stats built directly from exact probabilities (lse = 0, logit = log p):
+    every p used here is a dyadic rational whose exp(log p) round-trips exactly,
+    so a value placed on a threshold sits exactly on it."""
+    n = len(rows)
+    tid = np.zeros((n, k), dtype=np.int64)
+    tl = np.full((n, k), -np.inf)
+    for i, row in enumerate(rows):
+        items = sorted(row.items(), key=lambda kv: (-kv[1], kv[0]))
+        for j, (v, p) in enumerate(items):
+            assert math.exp(math.log(p)) == p, p
+            tid[i, j], tl[i, j] = v, math.log(p)
+        for j in range(len(items), k):
+            tid[i, j] = 40 + j                          # tokens of no mass (p = 0)
+    z = np.zeros(n)
+    return rps.Stats(H=z.copy(), lse=z, lmax=tl[:, 0].copy(), argmax=tid[:, 0].copy(), topk_id=tid, topk_logit=tl)
+
+
 def test_confidence_commit_threshold_inclusive():
-    st = planted([{1: 0.95}, {2: 0.9}, {3: 0.5}, {4: 0.89}])
-    rows, toks, _ = rps.confidence_commit(st, 0.9)
-    # 0.9 is representable only approximately; the row planted at 0.9 sits on the boundary
-    assert 0 in rows and 2 not in rows and 3 not in rows
-    assert all(t == r + 1 for r, t in zip(rows, toks))
+    # rows 0 and 2 sit exactly on tau = 0.5; a strict ">" would commit only the
+    # fallback row (one row) instead of both
+    st = dyadic([{1: 0.5, 9: 0.25}, {2: 0.375, 9: 0.25}, {3: 0.5, 9: 0.375}, {4: 0.25}])
+    assert np.all(confidence(st)[[0, 2]] == 0.5)
+    rows, toks, margin = rps.confidence_commit(st, 0.5)
+    assert rows.tolist() == [0, 2] and toks.tolist() == [1, 3]
+    assert margin == 0.0
+    rows, _, _ = rps.confidence_commit(st, 0.75)        # nothing reaches 0.75: fallback, lower row
+    assert rows.tolist() == [0]
 
 
 def test_confidence_commit_fallback_picks_most_confident_lowest_row():
@@ -119,13 +141,79 @@ def test_band_mode_picks_mid_entropy_rows():
     m_pos = np.arange(100, 121)
     prm = rps.Params(mode="band", k_max=10, pct_lo=25, pct_hi=75, n_pivots=3, r=0.0, n_cand=4)
     plan = rps.select_pivots(st, m_pos, prm)
-    lo, hi = np.percentile(st.H, 25), np.percentile(st.H, 75)
-    _, htr = rps.truncated(st, 10)
-    band = [j for j in range(21) if lo <= st.H[j] <= hi]
+    # expectation from the logits alone: scipy entropies and probabilities,
+    # numpy percentiles, and a plain loop over each row's 10 most probable tokens
+    p = scipy.special.softmax(logits, axis=1)
+    H = scipy.stats.entropy(p, axis=1)
+    lo, hi = np.percentile(H, 25), np.percentile(H, 75)
+    htr = []
+    for j in range(21):
+        top = sorted(range(V), key=lambda v: (-p[j, v], v))[:10]
+        htr.append(sum(-p[j, v] * math.log(p[j, v]) for v in top))
+    band = [j for j in range(21) if lo <= H[j] <= hi]
     expect = sorted(band, key=lambda j: (-htr[j], m_pos[j]))[:3]
     assert [p.row for p in plan.pivots] == expect
     assert all(len(p.tokens) == 4 for p in plan.pivots)
     assert all(p.tokens == st.topk_id[p.row, :4].tolist() for p in plan.pivots)
+
+
+# Row A keeps mass 0.9 on its top two tokens (0.5, 0.4); row B puts all its mass
+# on two tokens (0.5, 0.5).  Eq. 3's objective as printed (p not renormalised
+# over T_i) ranks A first: 0.5 ln 2 + 0.4 ln 2.5 = 0.7131 > ln 2.  Renormalised
+# over T_i, A would be (5/9, 4/9) with entropy 0.6870 < ln 2, and B would win.
+ROW_A = {3: 0.5, 4: 0.4}
+ROW_B = {5: 0.5, 6: 0.5}
+
+
+def _unnormalised_vs_renormalised():
+    def h(ps):
+        return -sum(q * math.log(q) for q in ps)
+    a, b = [0.5, 0.4], [0.5, 0.5]
+    un = (h(a), h(b))
+    re_ = (h([q / sum(a) for q in a]), h([q / sum(b) for q in b]))
+    assert un[0] > un[1] + 0.01 and re_[0] < re_[1] - 0.005     # the two readings disagree
+    return un
+
+
+@pytest.mark.parametrize("mode", ["paper", "band"])
+def test_truncated_entropy_is_not_renormalised(mode):
+    _unnormalised_vs_renormalised()
+    st = planted([ROW_B, ROW_A])
+    prm = rps.Params(mode=mode, k_max=2, tau_pivot=0.85, pct_lo=0, pct_hi=100, n_pivots=1, r=0.1)
+    plan = rps.select_pivots(st, np.array([20, 21]), prm)
+    assert [pv.pos for pv in plan.pivots] == [21]
+    assert plan.pivots[0].tokens == [3, 4]
+
+
+def test_pivot_mass_threshold_inclusive():
+    # row 0: top-2 mass 0.5 + 0.25 = 0.75 = tau_pivot exactly; row 1: 0.5 + 0.375
+    # is feasible too but has the lower truncated entropy; row 2: 0.25 + 0.25
+    st = dyadic([{1: 0.5, 2: 0.25}, {3: 0.5, 4: 0.375}, {5: 0.25, 6: 0.25, 7: 0.25}])
+    prm = rps.Params(mode="paper", k_max=2, tau_pivot=0.75, r=0.1)
+    mu, _ = rps.truncated(st, 2)
+    assert mu[0] == 0.75
+    plan = rps.select_pivots(st, np.array([7, 8, 9]), prm)
+    # truncated entropies: row 0: 0.5 ln 2 + 0.25 ln 4 = ln 2 = 0.693;
+    # row 1: 0.5 ln 2 + 0.375 ln(8/3) = 0.714  -> row 1 ranks first, row 0 second
+    assert [pv.row for pv in plan.pivots] == [1]
+    prm2 = rps.Params(mode="paper", k_max=2, tau_pivot=0.75, r=0.1, n_pivots=2)
+    plan2 = rps.select_pivots(st, np.array([7, 8, 9]), prm2)
+    assert [pv.row for pv in plan2.pivots] == [1, 0]
+    assert plan2.pivots[1].feas_margin == 0.0
+    # alone with an infeasible row, the boundary row is still the pivot
+    plan3 = rps.select_pivots(st.rows([0, 2]), np.array([7, 9]), prm)
+    assert [pv.pos for pv in plan3.pivots] == [7]
+
+
+def test_candidate_ratio_threshold_inclusive():
+    # p(v) / P^max = 0.25 / 0.5 = r exactly keeps the runner-up; a strict ">"
+    # would leave a single candidate and skip the pivot
+    st = dyadic([{1: 0.5, 2: 0.25, 3: 0.125 + 0.0625}, {4: 0.25, 5: 0.25}])
+    plan = rps.select_pivots(st, np.array([4, 5]), rps.Params(mode="paper", k_max=2, tau_pivot=0.5, r=0.5))
+    assert len(plan.pivots) == 1 and plan.pivots[0].tokens == [1, 2]
+    assert plan.pivots[0].cand_margin == 0.0
+    plan = rps.select_pivots(st, np.array([4, 5]), rps.Params(mode="paper", k_max=2, tau_pivot=0.5, r=0.5 + 2 ** -20))
+    assert plan.pivots == []
 
 
 # ------------------------------------------------------------ lookahead scoring
@@ -305,3 +393,20 @@ def test_branch_capacity_truncates_then_drops():
     # 4 + 4 fit, the third pivot keeps 1 candidate and is dropped, the fourth has none
     assert [len(p.tokens) for p in plan.pivots] == [4, 4]
     assert len(plan.branches()) == 8
+
+
+def test_band_edges_inclusive():
+    # with 5 rows the 25th and 75th percentiles (linear interpolation) are the
+    # 2nd and 4th order statistics exactly, so those two rows lie on the band's
+    # edges and stay feasible; a strict band would leave only the median row
+    rows = [{1: 0.5, 2: 0.25}, {3: 0.5, 4: 0.375}, {5: 0.25, 6: 0.25}, {7: 0.75, 8: 0.0625}, {9: 0.5, 10: 0.5}]
+    st = dyadic(rows)
+    st.H[:] = [4.0, 1.0, 3.0, 2.0, 5.0]          # edges: H = 2 (row 3) and H = 4 (row 0)
+    assert rps.percentile_linear(st.H, 25) == 2.0 and rps.percentile_linear(st.H, 75) == 4.0
+    prm = rps.Params(mode="band", k_max=2, pct_lo=25, pct_hi=75, n_pivots=3, r=0.0, n_cand=2)
+    plan = rps.select_pivots(st, np.arange(30, 35), prm)
+    # truncated entropies: row 0 ln 2 = 0.693, row 2 0.693 (0.25 ln 4 x 2), row 3
+    # 0.75 ln(4/3) + 0.0625 ln 16 = 0.389; ties go to the lower position
+    assert sorted(pv.row for pv in plan.pivots) == [0, 2, 3]
+    assert [pv.row for pv in plan.pivots] == [0, 2, 3]
+    assert min(pv.feas_margin for pv in plan.pivots) == 0.0
