@@ -176,7 +176,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
   // stays inside the source, and those keys are masked (K) or zeroed (V^T).
   auto issue = [&](int t, int slot) {
     const Src s = src(t);
-    const i32x4 rk = buffer_rsrc(s.k), rv = buffer_rsrc(s.v);
+    const rsrc_t rk = buffer_rsrc(s.k), rv = buffer_rsrc(s.v);
     const uint32_t base = lds0 + slot * C::STAGE;
 #pragma unroll
     for (int i = 0; i < C::IK; ++i) {

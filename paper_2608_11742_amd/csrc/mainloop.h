@@ -26,27 +26,25 @@
 
 namespace dllm {
 
-typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
-
-// Raw buffer resource (gfx9 layout: 48-bit base, stride 0, num_records,
-// word 3 = 32-bit data format) for a range starting at p.  num_records is the
-// maximum: every offset used with it is a clamped in-range row offset.
-__device__ __forceinline__ i32x4 buffer_rsrc(const void* p) {
-  const uint64_t a = reinterpret_cast<uint64_t>(p);
-  return i32x4{__builtin_amdgcn_readfirstlane(int(uint32_t(a))),
-               __builtin_amdgcn_readfirstlane(int(uint32_t(a >> 32) & 0xFFFF)), -1, 0x00020000};
+// Buffer resource for a range starting at p (stride 0, 32-bit data format):
+// num_records is the maximum, every offset used with it is a clamped
+// in-range row offset.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+__device__ __forceinline__ rsrc_t buffer_rsrc(const void* p) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), /*stride=*/0, /*num_records=*/-1,
+                                           /*flags=*/0x00020000);
 }
 
 // Asynchronous 16-byte-per-lane copy buffer -> LDS: lane l reads base +
 // voff + soff and writes LDS byte lds_addr + 16 l, where lds_addr is the
-// wave-uniform LDS address of the 1 KB block the 64 lanes fill.  Issued
-// through inline assembly so the compiler does not insert a conservative
-// wait for it before every LDS read; completion is awaited explicitly with
-// wait_vmcnt.
-__device__ __forceinline__ void lds_dma16(i32x4 rsrc, uint32_t voff, uint32_t soff, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %3\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(voff), "s"(rsrc), "s"(soff),
-               "s"(lds_addr)
-               : "memory", "m0");
+// wave-uniform LDS address of the 1 KB block the 64 lanes fill.  The
+// compiler's buffer-load-to-LDS builtin: it sets up M0 itself.  Completion
+// is awaited explicitly with wait_vmcnt before the barrier that publishes a
+// stage; the compiler does not wait for these copies before LDS reads.
+__device__ __forceinline__ void lds_dma16(rsrc_t rsrc, uint32_t voff, uint32_t soff, uint32_t lds_addr) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(
+      rsrc, reinterpret_cast<__attribute__((address_space(3))) void*>(static_cast<uintptr_t>(lds_addr)), 16, voff,
+      soff, 0, 0);
 }
 
 // s_waitcnt vmcnt(N) (expcnt and lgkmcnt left unconstrained)
@@ -58,6 +56,17 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 // s_waitcnt lgkmcnt(0) (vmcnt and expcnt left unconstrained)
 __device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt((0xF) | (0x3 << 14) | (0x7 << 4)); }
+
+// Workgroup barrier after this wave's LDS operations have completed, without
+// waiting for its outstanding copies into LDS (the workgroup fence of
+// __syncthreads would wait for those too).  The signal fences keep the
+// compiler from moving memory accesses across it.
+__device__ __forceinline__ void barrier_lds() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  wait_lgkmcnt0();
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
 
 // f(integral_constant<int, i>) for i = B .. E - 1, unrolled at compile time
 template <int B, int E, class F>
@@ -105,7 +114,7 @@ struct TileMma {
   struct Loader {
     uint32_t ga[kIA], gb[kIB];
     uint32_t lds0;
-    i32x4 ra, rb;
+    rsrc_t ra, rb;
     int wave;
     template <class AOff, class BOff>
     __device__ __forceinline__ Loader(uint8_t* smem, const uint8_t* A, const uint8_t* B, AOff a_off, BOff b_off) {
@@ -199,8 +208,8 @@ struct TileMma {
       ld.issue(0, 0);
       ld.issue(min(1, ns - 1), 1);
     }
-    wait_vmcnt<kIA + kIB>();   // stage 0 landed
-    __syncthreads();
+    wait_vmcnt<kIA + kIB>();   // stage 0 landed (stage 1 may still be in flight)
+    barrier_lds();
 #pragma unroll
     for (int m = 0; m < kFM; ++m) af[0][m] = a_frag(0, 0, m);
 #pragma unroll
