@@ -256,3 +256,165 @@ def model_prefix_cached(weights, shape, topk: int = 16, scales=None, scale: floa
 
         return (fwd, look) if packed else fwd
     return open_block
+
+
+# ------------------------------------------------------------ teacher forcing
+
+@dataclass
+class ForcedEvent:
+    """One decision of a followed trajectory: the oracle's own decision at
+    that point (made on the followed state) next to the one applied."""
+    kind: str                 # "commit", "skip" or "lookahead"
+    oracle: tuple             # the oracle's decision: ("commit", positions), ("skip",) or
+                              # ("lookahead", pivot, token or -1)
+    applied: tuple            # the followed (applied) decision, same form
+    margin: float             # the oracle's decision margin
+    token_rows: list = field(default_factory=list)   # (position, oracle argmax, applied token, argmax margin)
+
+
+def _commit_forced(state: rps.State, positions, tokens):
+    """Commit the given positions with the given tokens (the followed
+    trajectory's standard commit)."""
+    pos = np.asarray(sorted(positions), dtype=np.int64)
+    rows = np.nonzero(np.isin(state.m_pos, pos))[0]
+    assert rows.size == pos.size, "followed commit names positions outside M"
+    state.tokens[pos] = np.asarray([tokens[p] for p in pos], dtype=state.tokens.dtype)
+    keep = np.setdiff1d(np.arange(len(state.m_pos)), rows)
+    state.m_pos = state.m_pos[keep]
+    state.stats = state.stats.rows(keep)
+
+
+def rps_decode_follow(forward, prompt, gen_len: int, block: int, mask_id: int, prm: rps.Params, lam: float,
+                      tau: float, follow, final_tokens, capacity: int = 16, lookahead=None, block_forward=None):
+    """Algorithm 1 along a given trajectory (teacher forcing).
+
+    follow: the decisions of another implementation in order, ("commit",
+    positions), ("skip",) and ("lookahead", pivot, token or -1);
+    final_tokens: its final sequence (the token a commit wrote at each
+    position).  At every decision point the oracle makes its own decision on
+    the current state (the followed trajectory so far, with the oracle's own
+    forwards and carried distributions), records it with its margin, then
+    applies the followed decision, so that a near-tie does not change the
+    states that later decisions are made on.  Returns the list of
+    ForcedEvent."""
+    import dataclasses
+    prm = dataclasses.replace(prm, max_branch=min(prm.max_branch, capacity - 1))
+    prompt = np.asarray(prompt, dtype=np.int64)
+    final_tokens = np.asarray(final_tokens, dtype=np.int64)
+    P = len(prompt)
+    tokens = np.concatenate([prompt, np.full(gen_len, mask_id, dtype=np.int64)])
+    follow = list(follow)
+    events = []
+    it = iter(follow)
+    for b in range(gen_len // block):
+        m_pos = np.arange(P + b * block, P + (b + 1) * block)
+        m_pos = m_pos[tokens[m_pos] == mask_id]
+        stats = forward(tokens[None, :], m_pos, None)[0][0]
+        fb = None if block_forward is None else block_forward(tokens.copy(), P + b * block)
+        fwd_b, look_b = fb if isinstance(fb, tuple) else (fb or forward, lookahead)
+        state = rps.State(tokens, m_pos, stats)
+        while len(state.m_pos) > 0:
+            ev = next(it)
+            assert ev[0] == "commit", f"followed trajectory: expected a standard commit, got {ev}"
+            rows, toks, cmargin = rps.confidence_commit(state.stats, tau)
+            own = ("commit", tuple(sorted(int(state.m_pos[r]) for r in rows)))
+            applied = ("commit", tuple(sorted(int(p) for p in ev[1])))
+            # greedy tokens (Eq. 1) at the positions both sides commit
+            both = set(own[1]) & set(applied[1])
+            trow = [(int(state.m_pos[r]), int(state.stats.argmax[r]), int(final_tokens[state.m_pos[r]]),
+                     float(state.stats.argmax_margin[r]) if state.stats.argmax_margin is not None else np.inf)
+                    for r in range(len(state.m_pos)) if int(state.m_pos[r]) in both]
+            events.append(ForcedEvent("commit", own, applied, cmargin, trow))
+            _commit_forced(state, applied[1], final_tokens)
+            if len(state.m_pos) == 0:
+                break
+            ev = next(it)
+            plan = rps.select_pivots(state.stats, state.m_pos, prm)
+            plan.pivots = plan.pivots[:1]
+            brs = plan.branches()
+            if brs:
+                pv = plan.pivots[0]
+                batch = rps.branch_tokens(state.tokens, plan, with_anchor=True)
+                probe = [(pv.row, t) for t in pv.tokens]
+                outs = fwd_b(batch, state.m_pos, probe) if look_b is None else \
+                    look_b(batch, state.m_pos, probe, P + b * block, block)
+                anchor, anchor_probe = outs[0]
+                branch_stats = [o[0] for o in outs[1:]]
+                dec = rps.score(anchor, branch_stats, plan, lam, anchor_logp=anchor_probe)
+                pmargin = min(pv.feas_margin, pv.rank_margin, pv.cand_margin, plan.empty_margin)
+                own = ("lookahead", pv.pos, dec.token if dec.commit else -1)
+                margin = min(dec.margin_sum, pmargin)
+            else:
+                own, margin = ("skip",), plan.empty_margin
+            applied = tuple(ev)
+            events.append(ForcedEvent(own[0], own, applied, margin))
+            if applied[0] == "skip":
+                state.stats = fwd_b(state.tokens[None, :], state.m_pos, None)[0][0]
+                continue
+            assert applied[0] == "lookahead", applied
+            _, piv, tok = applied
+            prow = int(np.nonzero(state.m_pos == piv)[0][0])
+            # the followed lookahead's anchor and, on a commit, its winning
+            # branch, evaluated by the oracle as one lookahead batch
+            fplan = rps.Plan([rps.Pivot(row=prow, pos=int(piv), tokens=[int(tok)] if tok >= 0 else [],
+                                        logp=[0.0] if tok >= 0 else [])])
+            fbatch = rps.branch_tokens(state.tokens, fplan, with_anchor=True)
+            if tok >= 0 and brs and plan.pivots[0].pos == piv and int(tok) in plan.pivots[0].tokens:
+                win = branch_stats[plan.pivots[0].tokens.index(int(tok))]
+            elif tok < 0 and brs:
+                pass                                 # the anchor of the oracle's own lookahead
+            else:
+                fouts = fwd_b(fbatch, state.m_pos, None) if look_b is None else \
+                    look_b(fbatch, state.m_pos, None, P + b * block, block)
+                anchor = fouts[0][0]
+                win = fouts[1][0] if tok >= 0 else None
+            if tok >= 0:
+                state.tokens[piv] = tok
+                keep = np.array([j for j in range(len(state.m_pos)) if j != prow], dtype=np.int64)
+                state.m_pos = state.m_pos[keep]
+                state.stats = win.rows(keep)
+            else:
+                state.stats = anchor.rows(np.arange(len(anchor)))
+        tokens = state.tokens
+    assert next(it, None) is None, "followed trajectory has more decisions than the oracle's loop"
+    return events
+
+
+def baseline_decode_follow(forward, prompt, gen_len: int, block: int, mask_id: int, rule: str, k: int, tau: float,
+                           follow, final_tokens, block_forward=None):
+    """The baseline schedulers (Eq. 2) along a given trajectory of
+    ("commit", positions) steps: each step the oracle makes its own commit on
+    the followed state, records it with its margin, and applies the followed
+    commit.  Returns the list of ForcedEvent."""
+    prompt = np.asarray(prompt, dtype=np.int64)
+    final_tokens = np.asarray(final_tokens, dtype=np.int64)
+    P = len(prompt)
+    tokens = np.concatenate([prompt, np.full(gen_len, mask_id, dtype=np.int64)])
+    it = iter(list(follow))
+    events = []
+    for b in range(gen_len // block):
+        m_pos = np.arange(P + b * block, P + (b + 1) * block)
+        m_pos = m_pos[tokens[m_pos] == mask_id]
+        fwd_b = None
+        while len(m_pos) > 0:
+            stats = (forward if fwd_b is None else fwd_b)(tokens[None, :], m_pos, None)[0][0]
+            if fwd_b is None:
+                fb = forward if block_forward is None else block_forward(tokens.copy(), P + b * block)
+                fwd_b = fb[0] if isinstance(fb, tuple) else fb
+            state = rps.State(tokens, m_pos, stats)
+            if rule == "threshold":
+                rows, _, margin = rps.confidence_commit(stats, tau)
+            else:
+                rows, _, margin = rps.topk_commit(stats, rule, k)
+            own = ("commit", tuple(sorted(int(m_pos[r]) for r in rows)))
+            ev = next(it)
+            applied = ("commit", tuple(sorted(int(p) for p in ev[1])))
+            both = set(own[1]) & set(applied[1])
+            trow = [(int(m_pos[r]), int(stats.argmax[r]), int(final_tokens[m_pos[r]]),
+                     float(stats.argmax_margin[r]) if stats.argmax_margin is not None else np.inf)
+                    for r in range(len(m_pos)) if int(m_pos[r]) in both]
+            events.append(ForcedEvent("commit", own, applied, margin, trow))
+            _commit_forced(state, applied[1], final_tokens)
+            tokens, m_pos = state.tokens, state.m_pos
+    assert next(it, None) is None, "followed trajectory has more steps than the oracle's loop"
+    return events

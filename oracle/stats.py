@@ -73,16 +73,38 @@ def log_sum_exp(logits: np.ndarray) -> np.ndarray:
     return m + np.log(np.exp(logits - m[:, None]).sum(axis=1))
 
 
+def top_order(row: np.ndarray, n: int) -> np.ndarray:
+    """Indices of the n largest entries of a row, larger value first and the
+    lower index first on ties.  Every entry at least as large as the n-th
+    largest value is a candidate (so all entries tied with it are), and the
+    candidates are sorted by (-value, index)."""
+    V = row.shape[0]
+    if n >= V:
+        return np.lexsort((np.arange(V), -row))[:n]
+    thr = np.partition(row, V - n)[V - n]          # the n-th largest value
+    cand = np.nonzero(row >= thr)[0]
+    return cand[np.lexsort((cand, -row[cand]))][:n]
+
+
 def softmax_stats(logits: np.ndarray, topk: int) -> Stats:
-    """Statistics of each row of logits ([R, V], -inf marks excluded tokens)."""
+    """Statistics of each row of logits ([R, V], -inf marks excluded tokens).
+
+    Rows are processed 16 at a time: every row's statistics depend on that
+    row alone, and small blocks keep the temporaries in reused heap memory."""
     logits = np.asarray(logits, dtype=np.float64)
+    if logits.shape[0] > 16:
+        return Stats.concat([_stats_block(logits[i:i + 16], topk) for i in range(0, logits.shape[0], 16)])
+    return _stats_block(logits, topk)
+
+
+def _stats_block(logits: np.ndarray, topk: int) -> Stats:
     R, V = logits.shape
     lmax = logits.max(axis=1)
     lse = log_sum_exp(logits)
     H = entropy_from_logits(logits)
-    ids = np.arange(V)
-    # order: larger logit first, then smaller token id
-    order = np.stack([np.lexsort((ids, -row)) for row in logits])
+    # order: larger logit first, then smaller token id; only the first
+    # topk + 1 ranks are needed
+    order = np.stack([top_order(row, min(V, max(topk + 1, 2))) for row in logits])
     top = order[:, :topk]
     top_logit = np.take_along_axis(logits, top, axis=1)
     nxt = np.take_along_axis(logits, order[:, 1:2], axis=1)[:, 0]

@@ -12,7 +12,7 @@ from synth import workloads as W
 from oracle import model as om
 from oracle import rps as orps
 from oracle.stats import softmax_stats
-from tests.parity import compare_stats, MARGIN
+from tests.parity import compare_stats, MARGIN, perturbed, allowed_flips, flip_rows
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -30,16 +30,22 @@ def lm_head():
     return synth.weight_torch(W.SEED_WEIGHTS, "lm_head", (B8.vocab, B8.d_model), dtype="bf16", device=DEV)
 
 
-@pytest.mark.parametrize("R", [4096, 4000])
-def test_lm_head_stats_full_shape_sampled_rows(P, lm_head, R):
-    """vocab_entropy_topk at the step's LM-head shape; 24 sampled rows against the oracle."""
+@pytest.mark.parametrize("R", [1, 16, 31, 32, 128, 129, 4000, 4096])
+def test_lm_head_stats_full_shape(P, lm_head, R):
+    """vocab_entropy_topk with the 8B LM head (d 4096, V 126464).  Up to 129
+    rows (one or two 128-row tiles over all vocabulary slices, the multi-wave
+    merge of a decode's block forwards) every row is compared; at the step's
+    4096 (and a ragged 4000) rows, 24 sampled rows."""
     h = synth.weight_torch(21, "hidden", (R, B8.d_model), std=1.0, dtype="bf16", device=DEV)
     rs = torch.from_numpy((0.5 + 3 * synth.uniform01_np(22, "rs", R)).astype(np.float32)).to(DEV)
     out = P.Stats(R, 16, device=DEV)
     ws = torch.empty(P.vocab_entropy_topk_workspace_bytes(R, B8.vocab), dtype=torch.uint8, device=DEV)
     P.vocab_entropy_topk(h, lm_head, out, ws, row_scale=rs, scale=1.0, mask_id=B8.mask_id)
     torch.cuda.synchronize()
-    rows = np.unique(np.concatenate([[0, 1, 127, 128, R - 1], synth.tokens_np(23, "rows", 19, R)]))
+    if R <= 256:
+        rows = np.arange(R)
+    else:
+        rows = np.unique(np.concatenate([[0, 1, 127, 128, R - 1], synth.tokens_np(23, "rows", 19, R)]))
     hn = h[torch.from_numpy(rows).to(DEV)].float().cpu().numpy().astype(np.float64)
     wn = lm_head.float().cpu().numpy().astype(np.float64)
     logits = rs.cpu().numpy()[rows].astype(np.float64)[:, None] * (hn @ wn.T)
@@ -77,12 +83,16 @@ def test_two_layer_8b_width_forward_in_bench_launch_config(P, b8_two_layer):
     out = model.forward(torch.from_numpy(batch).to(DEV), torch.from_numpy(m_pos).to(DEV), scale=1.0)
     torch.cuda.synchronize()
     b = 5
-    w_np = {k: v.float().cpu().numpy() for k, v in w.items()}
+    w_np = {k: v.double().cpu().numpy() for k, v in w.items()}
     sample = np.unique(np.concatenate([[0, 255], synth.tokens_np(33, "s", 30, 256)]))
-    h = om.hidden(batch[b], w_np, shape, mirror=True)[m_pos[sample]]
-    ref = softmax_stats(om.lm_logits(h, w_np, shape, scale=1.0), 16)
+
+    def oracle(wts):
+        h = om.hidden(batch[b], wts, shape, mirror=True)[m_pos[sample]]
+        return softmax_stats(om.lm_logits(h, wts, shape, scale=1.0), 16)
+    ref, ref2 = oracle(w_np), oracle(perturbed(w_np))
     got = {k: v[b * 256 + sample] for k, v in out.numpy().items()}
-    print(compare_stats(got, ref, 2e-2, margin="auto", label="2-layer 8B width"))
+    print(compare_stats(got, ref, 2e-2, label="2-layer 8B width", max_exceptions=allowed_flips(ref, ref2),
+                        id_ranks=4), "oracle's own flips", flip_rows(ref, ref2))
 
 
 def test_batch_invariance(P, b8_two_layer):
@@ -181,17 +191,28 @@ def test_cached_step_two_layer_8b_width(P, b8_two_layer):
     out = model_p.forward(torch.from_numpy(blocks).to(DEV), torch.from_numpy(lm).to(DEV), pos_offset=Pn,
                           kv_prefix=kv, scale=1.0)
     torch.cuda.synchronize()
-    w_np = {kk: v.float().cpu().numpy() for kk, v in w.items()}
-    ref_kv = om.prefix_cache(prefix, w_np, shape, mirror=True)
+    w_np = {kk: v.double().cpu().numpy() for kk, v in w.items()}
     b = 7
-    h = om.hidden(blocks[b], w_np, shape, pos_offset=Pn, mirror=True, prefix_kv=ref_kv)
-    ref = softmax_stats(om.lm_logits(h, w_np, shape, scale=1.0), 16)
+
+    def oracle_stats(wts):
+        kv_ = om.prefix_cache(prefix, wts, shape, mirror=True)
+        h = om.hidden(blocks[b], wts, shape, pos_offset=Pn, mirror=True, prefix_kv=kv_)
+        return softmax_stats(om.lm_logits(h, wts, shape, scale=1.0), 16)
+    ref = oracle_stats(w_np)
     got = {kk: v[b * Bk:(b + 1) * Bk] for kk, v in out.numpy().items()}
-    # Individual logits of this model are at the oracle's own noise floor:
-    # perturbing the mirror oracle by a relative 1e-7 (about one float32 ulp)
-    # at its bfloat16 rounding points moves branch 7's top-1 logits by
-    # 1.9e-2, by 1e-6 by 2.4e-2 (two random layers amplify rounding-order
-    # differences over 1056 keys; entropies move by 4e-4).  Logits therefore
-    # get 3e-2 here; entropies and log-partition values keep 2e-2.
-    print(compare_stats(got, ref, 2e-2, margin="auto", label="cached step 2-layer 8B width", logit_tol=3e-2))
+    # The oracle's own rounding-order noise floor on this model: the same
+    # mirror oracle with every layer weight perturbed by a relative 1e-6
+    # (random signs; the size of float32 accumulation error over 4096 terms)
+    # moves individual logits by `spread`, since two random layers over 1056
+    # keys amplify flips of bf16 rounding decisions.  Individual logits (lmax,
+    # top-k logits) are held to max(2e-2, 1.25 x spread); entropies and
+    # log-partition values keep 2e-2.
+    ref2 = oracle_stats(perturbed(w_np))
+    spread = max(float(np.max(np.abs(ref.lmax - ref2.lmax))),
+                 float(np.max(np.abs(ref.topk_logit - ref2.topk_logit))))
+    logit_tol = max(2e-2, 1.25 * spread)
+    rep = compare_stats(got, ref, 2e-2, label="cached step 2-layer 8B width", logit_tol=logit_tol,
+                        max_exceptions=allowed_flips(ref, ref2), id_ranks=4)
+    print(f"oracle noise floor {spread:.3e}, logit bound {logit_tol:.3e}, oracle's own flips {flip_rows(ref, ref2)}",
+          rep)
     model_p.close()

@@ -217,3 +217,78 @@ def test_packed_lookahead_over_the_cache_decode_invariants():
                      block_forward=model_prefix_cached(w, shape, scales=scales, packed=True))
     _check_trace(res, P, G, B, shape.mask_id)
     assert res.nfe == res.normal + res.lookahead and res.nfe <= G
+
+
+# ------------------------------------------------------------ teacher forcing
+
+from oracle.decode import rps_decode_follow, baseline_decode, baseline_decode_follow  # noqa: E402
+
+_F_SHAPE = synth.ModelShape(n_layers=2, d_model=64, n_heads=4, head_dim=16, d_ffn=96, vocab=101)
+
+
+def _own_key(e):
+    return ("commit", tuple(e[1])) if e[0] == "commit" else tuple(e[:-1])
+
+
+@pytest.mark.parametrize("variant", ["plain", "packed", "prefix_cache"])
+def test_following_its_own_trajectory_reproduces_every_decision(variant):
+    w = synth.model_weights_np(_F_SHAPE, seed=7, dtype="f32")
+    P, G, B = 8, 32, 16
+    prompt = synth.tokens_np(8, "prompt", P, _F_SHAPE.vocab - 1)
+    scales = synth.position_scales_np(9, np.arange(P + G), 2.6, 16.0)
+    prm = rps.Params(mode="paper", k_max=8, tau_pivot=0.5, r=0.05, n_cand=8)
+    fwd = model_forward(w, _F_SHAPE, scales=scales)
+    kw = {}
+    if variant == "packed":
+        kw["lookahead"] = model_packed_lookahead(w, _F_SHAPE, scales=scales)
+    elif variant == "prefix_cache":
+        kw["block_forward"] = model_prefix_cached(w, _F_SHAPE, scales=scales)
+    res = rps_decode(fwd, prompt, G, B, _F_SHAPE.mask_id, prm, lam=0.1, tau=0.9, **kw)
+    follow = [("commit", t[1]) if t[0] == "commit" else (("skip",) if t[0] == "skip" else tuple(t[:-1]))
+              for t in res.trace]
+    ev = rps_decode_follow(fwd, prompt, G, B, _F_SHAPE.mask_id, prm, 0.1, 0.9, follow, res.tokens, **kw)
+    assert res.lookahead > 0
+    assert len(ev) == len(res.trace)
+    for e, t in zip(ev, res.trace):
+        assert e.oracle == e.applied
+        assert e.oracle == _own_key(t)
+        assert e.margin == t[-1]
+        assert all(own == app for _, own, app, _ in e.token_rows)
+
+
+def test_following_another_trajectory_records_the_differences():
+    # a valid trajectory of a differently scaled model, followed with the
+    # original: the follower takes every step of it (its own decision may
+    # differ, the applied one is the other's) and finishes the sequence
+    w = synth.model_weights_np(_F_SHAPE, seed=7, dtype="f32")
+    P, G, B = 8, 32, 16
+    prompt = synth.tokens_np(8, "prompt", P, _F_SHAPE.vocab - 1)
+    scales = synth.position_scales_np(9, np.arange(P + G), 2.6, 16.0)
+    prm = rps.Params(mode="paper", k_max=8, tau_pivot=0.5, r=0.05, n_cand=8)
+    other = rps_decode(model_forward(w, _F_SHAPE, scales=scales * 1.3), prompt, G, B, _F_SHAPE.mask_id, prm,
+                       lam=0.1, tau=0.9)
+    follow = [("commit", t[1]) if t[0] == "commit" else (("skip",) if t[0] == "skip" else tuple(t[:-1]))
+              for t in other.trace]
+    fwd = model_forward(w, _F_SHAPE, scales=scales)
+    ev = rps_decode_follow(fwd, prompt, G, B, _F_SHAPE.mask_id, prm, 0.1, 0.9, follow, other.tokens)
+    assert len(ev) == len(other.trace)
+    assert [e.applied for e in ev] == [("commit", tuple(f[1])) if f[0] == "commit" else tuple(f) for f in follow]
+    assert any(e.oracle != e.applied for e in ev)
+    # the first decision is made on the same state by both and differs only if the models disagree
+    own = rps_decode(fwd, prompt, G, B, _F_SHAPE.mask_id, prm, lam=0.1, tau=0.9)
+    assert ev[0].oracle == _own_key(own.trace[0])
+
+
+@pytest.mark.parametrize("rule,k,tau", [("confidence", 2, 0.0), ("entropy", 3, 0.0), ("threshold", 1, 0.6)])
+def test_baseline_following_its_own_trajectory(rule, k, tau):
+    w = synth.model_weights_np(_F_SHAPE, seed=7, dtype="f32")
+    P, G, B = 8, 32, 16
+    prompt = synth.tokens_np(8, "prompt", P, _F_SHAPE.vocab - 1)
+    scales = synth.position_scales_np(9, np.arange(P + G), 2.6, 16.0)
+    fwd = model_forward(w, _F_SHAPE, scales=scales)
+    res = baseline_decode(fwd, prompt, G, B, _F_SHAPE.mask_id, rule, k, tau=tau)
+    ev = baseline_decode_follow(fwd, prompt, G, B, _F_SHAPE.mask_id, rule, k, tau,
+                                [("commit", t[1]) for t in res.trace], res.tokens)
+    assert len(ev) == len(res.trace)
+    for e, t in zip(ev, res.trace):
+        assert e.oracle == e.applied == ("commit", tuple(t[1])) and e.margin == t[2]
