@@ -218,6 +218,25 @@ dllm_status vocab_entropy_topk(const void* hidden, const void* w_lm, int32_t R, 
                                int32_t dtype, const float* row_scale, float scale, int32_t mask_id,
                                const dllm_stats* out, void* ws, size_t ws_bytes, dllm_stream stream);
 
+/* Allocation-free variant of vocab_entropy_topk, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same kernels and results, with the
+ * partial statistics in a device scratch array that the library holds on
+ * every device it runs on (DLLM_NOALLOC_SCRATCH_BYTES, until the process
+ * ends) instead of a caller workspace.  Arguments as vocab_entropy_topk; the
+ * caller still owns hidden, w_lm, row_scale and out.  The device is the
+ * stream's (the current device for the NULL stream); the first call on a
+ * device looks the scratch up (hipGetSymbolAddress), no call allocates.
+ * All calls on one device share its scratch: calls that overlap on one
+ * device (concurrent streams, threads) race and must be serialised by the
+ * caller.  Errors: those of vocab_entropy_topk, and DLLM_ENOMEM when
+ * vocab_entropy_topk_workspace_bytes(R, vocab) exceeds the scratch
+ * (beyond about 180 000 rows). */
+#define DLLM_NOALLOC_SCRATCH_BYTES (48u << 20)
+dllm_status vocab_entropy_topk_noalloc(const void* hidden, const void* w_lm, int32_t R, int32_t d, int32_t vocab,
+                                       int32_t dtype, const float* row_scale, float scale, int32_t mask_id,
+                                       const dllm_stats* out, dllm_stream stream);
+
 /* Kernel timing for benchmarks.  Between dllm_profile_begin and
  * dllm_profile_end every kernel that dllm_forward launches is bracketed by
  * HIP events on the launch stream (for at most max_launches launches).

@@ -8,7 +8,7 @@ Importing the package loads the library and fails if it is not built.
 from . import binding  # noqa: F401
 from .binding import (  # noqa: F401
     Stats, dllm_model_create, dllm_model_destroy, dllm_workspace_bytes, dllm_forward, dllm_forward_packed,
-    vocab_entropy_topk, vocab_entropy_topk_workspace_bytes, rps_select_pivots, rps_build_branches, rps_build_packed,
+    vocab_entropy_topk, vocab_entropy_topk_noalloc, vocab_entropy_topk_workspace_bytes, rps_select_pivots, rps_build_branches, rps_build_packed,
     dllm_workspace_bytes_packed,
     rps_lookahead_score, rps_commit, sched_commit, params, new_plan, new_decision, read_plan, read_decision, lib,
     dllm_profile_begin, dllm_profile_end,

@@ -85,6 +85,7 @@ SIGNATURES = {
                                   C.POINTER(Probe), C.POINTER(StatsC), vp, sz, vp]),
     "vocab_entropy_topk_workspace_bytes": (sz, [i32, i32]),
     "vocab_entropy_topk": (i32, [vp, vp, i32, i32, i32, i32, vp, f32, i32, C.POINTER(StatsC), vp, sz, vp]),
+    "vocab_entropy_topk_noalloc": (i32, [vp, vp, i32, i32, i32, i32, vp, f32, i32, C.POINTER(StatsC), vp]),
     "dllm_profile_begin": (i32, [vp, i32]),
     "dllm_profile_begin_classes": (i32, [vp, i32, C.c_uint32]),
     "dllm_profile_end": (i32, [vp, C.POINTER(f32), C.POINTER(i32)]),

@@ -198,6 +198,15 @@ def vocab_entropy_topk(hidden, w_lm, out: Stats, ws, row_scale=None, scale: floa
                                     C.byref(out.c()), _p(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
+def vocab_entropy_topk_noalloc(hidden, w_lm, out: Stats, row_scale=None, scale: float = 1.0, mask_id: int = -1,
+                               stream=None):
+    R, d = hidden.shape
+    V = w_lm.shape[0]
+    dt = DLLM_BF16 if hidden.dtype == torch.bfloat16 else DLLM_F32
+    _check(lib().vocab_entropy_topk_noalloc(_p(hidden), _p(w_lm), R, d, V, dt, _p(row_scale), scale, mask_id,
+                                            C.byref(out.c()), _stream(stream)))
+
+
 # ---------------------------------------------------------------- scheduler
 
 def rps_select_pivots(base: Stats, m_pos, n_m: int, prm: RpsParams, plan, stream=None):

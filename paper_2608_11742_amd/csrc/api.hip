@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -502,6 +503,66 @@ dllm_status vocab_entropy_topk(const void* hidden, const void* w_lm, int32_t R, 
   TRY_HIP(lmhead_partials(dtype, hidden, w_lm, R, d, vocab, row_scale, nullptr, R, R, scale, mask_id, ws, s),
           "vocab_entropy_topk");
   return hip_check(lmhead_merge(R, vocab, to_out(*out), ws, s), "vocab_entropy_topk merge");
+}
+
+// ---------------------------------------------------------------- allocation-free LM head
+
+// Partial statistics of vocab_entropy_topk_noalloc, held by every device the
+// library runs on until the process ends.  Host code never passes the array's
+// name to a kernel (on the host it is only a stand-in for the symbol): the
+// device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) uint8_t scratch[DLLM_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// Device address of `scratch` on device `dev`, looked up on the first call
+// for that device with the device current.
+dllm_status scratch_address(int dev, void** out) {
+  if (dev < 0 || dev >= kMaxDevices) return fail(DLLM_EUNSUPPORTED, "device %d beyond %d devices", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    int cur = -1;
+    TRY_HIP(hipGetDevice(&cur), "hipGetDevice");
+    if (cur != dev) TRY_HIP(hipSetDevice(dev), "hipSetDevice");
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    TRY_HIP(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(DLLM_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return DLLM_OK;
+}
+
+}  // namespace
+
+dllm_status vocab_entropy_topk_noalloc(const void* hidden, const void* w_lm, int32_t R, int32_t d, int32_t vocab,
+                                       int32_t dtype, const float* row_scale, float scale, int32_t mask_id,
+                                       const dllm_stats* out, dllm_stream stream) {
+  if (R < 1 || vocab < 2) return fail(DLLM_ESHAPE, "R %d vocab %d", R, vocab);
+  const size_t need = lmhead_workspace(R, vocab);
+  if (need > size_t(DLLM_NOALLOC_SCRATCH_BYTES))
+    return fail(DLLM_ENOMEM, "vocab_entropy_topk_noalloc: R %d x vocab %d needs %zu bytes of partials, beyond the "
+                "%zu-byte device scratch", R, vocab, need, size_t(DLLM_NOALLOC_SCRATCH_BYTES));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int dev = -1;
+  if (s) {
+    TRY_HIP(hipStreamGetDevice(s, &dev), "hipStreamGetDevice");
+  } else {
+    TRY_HIP(hipGetDevice(&dev), "hipGetDevice");
+  }
+  void* ws = nullptr;
+  dllm_status st = scratch_address(dev, &ws);
+  if (st != DLLM_OK) return st;
+  // every partial slot the merge reads is written by the partials kernel of
+  // the same call: nothing in the scratch has to start at zero
+  return vocab_entropy_topk(hidden, w_lm, R, d, vocab, dtype, row_scale, scale, mask_id, out, ws,
+                            size_t(DLLM_NOALLOC_SCRATCH_BYTES), stream);
 }
 
 dllm_status rps_select_pivots(const dllm_stats* base, const int32_t* m_pos, int32_t n_m, const rps_params* prm,
