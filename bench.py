@@ -131,7 +131,19 @@ def cpu_baseline(wl, w_dev, tokens_np, m_pos_np, n_layers_sample=16, lm_rows_sam
                        f"({t_layers:.2f} s) and the LM head + statistics on {lm_rows_sample} of its {n_m} "
                        f"masked rows ({t_lm:.2f} s), scaled x{n_branch} branches, x{shape.n_layers} layers, "
                        f"x{n_m} rows to one step ({t_step:.1f} s)"),
-            "sample_seconds": round(t_layers + t_lm, 2), "host_cpus": os.cpu_count()}
+            "sample_seconds": round(t_layers + t_lm, 2), "host_cpus": os.cpu_count(), "cpu_model": cpu_model()}
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (the first "model name" line of /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def timed(fn, n):
