@@ -108,10 +108,10 @@ GemmSplits plan_gemms(const dllm_model_desc& d, int M) {
   auto cdiv = [](int a, int b) { return (a + b - 1) / b; };
   const int tq = cdiv(3 * d.d_model, 256), to = cdiv(d.d_model, 256), tg = cdiv(d.d_ffn, 128);
   GemmSplits g;
-  g.qkv = gemm_splits(M, tq, d.d_model, dt);
-  g.o = gemm_splits(M, to, d.d_model, dt);
-  g.gu = d.d_ffn % 4 ? 1 : gemm_splits(M, tg, d.d_model, dt);
-  g.down = gemm_splits(M, to, d.d_ffn, dt);
+  g.qkv = gemm_splits(GEMM_KIND_QKV, M, 3 * d.d_model, d.d_model, dt);
+  g.o = gemm_splits(GEMM_KIND_RESID, M, d.d_model, d.d_model, dt);
+  g.gu = d.d_ffn % 4 ? 1 : gemm_splits(GEMM_KIND_GATEUP, M, 2 * d.d_ffn, d.d_model, dt);
+  g.down = gemm_splits(GEMM_KIND_RESID, M, d.d_model, d.d_ffn, dt);
   g.bytes = std::max(std::max(gemm_partial_bytes(M, tq, g.qkv), gemm_partial_bytes(M, to, g.o)),
                      std::max(gemm_partial_bytes(M, tg, g.gu), gemm_partial_bytes(M, to, g.down)));
   return g;

@@ -28,6 +28,11 @@ struct GemmCfg {
 };
 using Big = GemmCfg<256, 256, 4, 2, 2>;
 using Small = GemmCfg<64, 256, 1, 2, 2>;
+// few rows (a block forward over a cached prefix, the suffix of a decode):
+// 128 x 256 tiles of 8 waves of 32 x 128 (two per SIMD, as Big), so that a
+// 65-256-row projection wastes fewer clamped rows and needs half the split-K
+// parts of 256-row tiles
+using Quad = GemmCfg<128, 256, 4, 2, 1>;
 // gate/up with 257-512 rows: 256 x 192 tiles (waves of 64 x 96, 48 gate + 48
 // up rows each) give 2 x F / 96 = 256 workgroups for the 8B shape, one per CU,
 // where 256 x 256 tiles leave a quarter of the CUs idle
@@ -38,6 +43,15 @@ constexpr int kGroupM = 8;
 #define DLLM_SMALL_M_MAX 64
 #endif
 constexpr int kSmallM = DLLM_SMALL_M_MAX;
+
+// Row tile of a projection of M rows: Small up to kSmallM rows; Quad where it
+// measured faster than Big (the d-wide O projection up to 512 rows, the
+// F-deep down projection up to 192, QKV and gate/up up to 128); Big above.
+int tile_rows(int kind, int M, int N, int K) {
+  if (M <= kSmallM) return Small::BM;
+  const int quad_max = kind == GEMM_KIND_RESID ? (K <= N ? 512 : 192) : 128;
+  return M <= quad_max ? Quad::BM : Big::BM;
+}
 
 // EPI_PART / EPI_PART_GU: split-K partial tiles (GU: the gate/up row pairing
 // of EPI_SWIGLU) written to part[split][M][np]
@@ -194,27 +208,29 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
   if constexpr (kSplit) {
     // the fp32 partial tile through LDS as in the residual epilogue, 16-byte
     // stores along rows of part[split]
-    static_assert(TM::kWTM % 64 == 0 && TM::kWTN == 128, "partial epilogue tiling");
-    uint8_t* st = smem + wave * (64 * 64 * 4);
+    static_assert((TM::kWTM % 64 == 0 || TM::kWTM == 32) && TM::kWTN == 128, "partial epilogue tiling");
+    constexpr int RG = TM::kWTM >= 64 ? 64 : TM::kWTM;   // rows per staged group
+    static_assert(TM::kWaves * RG * 64 * 4 <= TM::kSmem, "staging inside the ring");
+    uint8_t* st = smem + wave * (RG * 64 * 4);
     auto slot_of = [](int r, int c4) { return r * 256 + (((c4 ^ (r & 15))) << 4); };
     float* P = ep.part + size_t(part) * M * ep.np;
 #pragma unroll
-    for (int g = 0; g < TM::kWTM / 64; ++g) {   // 64-row groups of the wave tile
-      const int r0 = m0 + wm * TM::kWTM + 64 * g;
+    for (int g = 0; g < TM::kWTM / RG; ++g) {   // row groups of the wave tile
+      const int r0 = m0 + wm * TM::kWTM + RG * g;
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
 #pragma unroll
-        for (int m = 0; m < 4; ++m)
+        for (int m = 0; m < RG / 16; ++m)
 #pragma unroll
           for (int nn = 0; nn < 4; ++nn)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const int r = m * 16 + 4 * (lane >> 4) + i, c = nn * 16 + lc;
-              *reinterpret_cast<float*>(st + slot_of(r, c >> 2) + (c & 3) * 4) = acc[4 * g + m][4 * h + nn][i];
+              *reinterpret_cast<float*>(st + slot_of(r, c >> 2) + (c & 3) * 4) = acc[(RG / 16) * g + m][4 * h + nn][i];
             }
         const int c0 = tn * Cfg::BN + wn * TM::kWTN + 64 * h;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
+        for (int j = 0; j < RG / 4; ++j) {
           const int q = lane + 64 * j, r = q >> 4, c4 = q & 15;
           const int row = r0 + r;
           if (row < M)
@@ -230,33 +246,35 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
     // both the MFMA-layout writes and the row reads are conflict-free; then
     // every lane reads 16 bytes of x per access, all loads first (clamped
     // into the matrix) and the guarded stores after them.
-    static_assert(TM::kWTM % 64 == 0 && TM::kWTN == 128, "resid epilogue tiling");
-    uint8_t* st = smem + wave * (64 * 64 * 4);
+    static_assert((TM::kWTM % 64 == 0 || TM::kWTM == 32) && TM::kWTN == 128, "resid epilogue tiling");
+    constexpr int RG = TM::kWTM >= 64 ? 64 : TM::kWTM;   // rows per staged group
+    static_assert(TM::kWaves * RG * 64 * 4 <= TM::kSmem, "staging inside the ring");
+    uint8_t* st = smem + wave * (RG * 64 * 4);
     auto slot_of = [](int r, int c4) { return r * 256 + (((c4 ^ (r & 15))) << 4); };
 #pragma unroll
-    for (int g = 0; g < TM::kWTM / 64; ++g) {   // 64-row groups of the wave tile
-      const int r0 = m0 + wm * TM::kWTM + 64 * g;
+    for (int g = 0; g < TM::kWTM / RG; ++g) {   // row groups of the wave tile
+      const int r0 = m0 + wm * TM::kWTM + RG * g;
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
 #pragma unroll
-        for (int m = 0; m < 4; ++m)
+        for (int m = 0; m < RG / 16; ++m)
 #pragma unroll
           for (int nn = 0; nn < 4; ++nn)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const int r = m * 16 + 4 * (lane >> 4) + i, c = nn * 16 + lc;
-              *reinterpret_cast<float*>(st + slot_of(r, c >> 2) + (c & 3) * 4) = acc[4 * g + m][4 * h + nn][i];
+              *reinterpret_cast<float*>(st + slot_of(r, c >> 2) + (c & 3) * 4) = acc[(RG / 16) * g + m][4 * h + nn][i];
             }
         const int c0 = tn * Cfg::BN + wn * TM::kWTN + 64 * h;
-        f32x4 xv[16];
+        f32x4 xv[RG / 4];
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
+        for (int j = 0; j < RG / 4; ++j) {
           const int q = lane + 64 * j, r = q >> 4, c4 = q & 15;
           const int row = min(r0 + r, M - 1), col = min(c0 + 4 * c4, N - 4);
           xv[j] = *reinterpret_cast<const f32x4*>(ep.x + size_t(row) * ep.ldx + col);
         }
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
+        for (int j = 0; j < RG / 4; ++j) {
           const int q = lane + 64 * j, r = q >> 4, c4 = q & 15;
           const int row = r0 + r, col = c0 + 4 * c4;
           const f32x4 a = *reinterpret_cast<const f32x4*>(st + slot_of(r, c4));
@@ -310,6 +328,7 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
         // back only what it wrote: its LDS operations complete in order, so
         // no barrier.
         static_assert(TM::kWTN == 128, "qkv staging: 16 chunks per row");
+        static_assert(TM::kWaves * TM::kWTM * TM::kWTN * 2 <= TM::kSmem, "qkv staging inside the ring");
         uint8_t* st = smem + wave * (TM::kWTM * TM::kWTN * 2);
         auto off = [](int r, int c16) { return r * 256 + ((c16 ^ (((r >> 2) & 3) << 1)) << 4); };
 #pragma unroll
@@ -449,11 +468,13 @@ hipError_t launch_cfg(const void* A, int lda, const void* B, int ldb, int M, int
   return hipGetLastError();
 }
 
+// bm: the row tile (tile_rows)
 template <typename T, int EPI, int HD = 0>
-hipError_t launch(const void* A, int lda, const void* B, int ldb, int M, int N, int K, int tiles_n,
+hipError_t launch(int bm, const void* A, int lda, const void* B, int ldb, int M, int N, int K, int tiles_n,
                   const EpiParams& ep, hipStream_t s, int splits = 1) {
-  return M <= kSmallM ? launch_cfg<T, EPI, HD, Small>(A, lda, B, ldb, M, N, K, tiles_n, ep, s, splits)
-                      : launch_cfg<T, EPI, HD, Big>(A, lda, B, ldb, M, N, K, tiles_n, ep, s, splits);
+  if (bm == Small::BM) return launch_cfg<T, EPI, HD, Small>(A, lda, B, ldb, M, N, K, tiles_n, ep, s, splits);
+  if (bm == Quad::BM) return launch_cfg<T, EPI, HD, Quad>(A, lda, B, ldb, M, N, K, tiles_n, ep, s, splits);
+  return launch_cfg<T, EPI, HD, Big>(A, lda, B, ldb, M, N, K, tiles_n, ep, s, splits);
 }
 
 // ---------------------------------------------------------------- split-K reductions
@@ -611,10 +632,11 @@ hipError_t splitk_add(const SplitK& sk, int M, int N, float* X, int ldx, hipStre
   return hipGetLastError();
 }
 
-int gemm_splits(int M, int tiles_n, int K, int dtype) {
-  // workgroups that fill the 256 CUs: one 256-row workgroup per CU, two small ones
-  const bool small = M <= kSmallM;
-  const int tiles = cdiv(M, small ? Small::BM : Big::BM) * tiles_n, full = small ? 512 : 256;
+int gemm_splits(int kind, int M, int N, int K, int dtype) {
+  // workgroups that fill the 256 CUs: one Big or Quad workgroup per CU, two Small ones
+  const int bm = tile_rows(kind, M, N, K);
+  const int tiles_n = kind == GEMM_KIND_GATEUP ? cdiv(N / 2, 128) : cdiv(N, kBN);
+  const int tiles = cdiv(M, bm) * tiles_n, full = bm == Small::BM ? 512 : 256;
   const int stages = K / (dtype ? 64 : 32);   // 128-byte K stages
   if (tiles >= full * 5 / 8 || stages < 2) return 1;
   const int parts = std::max(1, std::min(full / tiles, stages / 4));
@@ -637,16 +659,17 @@ hipError_t gemm_resid(int dtype, const void* A, int lda, const void* B, int ldb,
   ep.x = X;
   ep.ldx = ldx;
   const int tn = cdiv(N, kBN);
+  const int bm = tile_rows(GEMM_KIND_RESID, M, N, K);
   if (sk && sk->splits > 1) {
     ep.part = sk->part;
     ep.np = tn * kBN;
-    hipError_t e = dtype ? launch<bf16_t, EPI_PART>(A, lda, B, ldb, M, N, K, tn, ep, s, sk->splits)
-                         : launch<float, EPI_PART>(A, lda, B, ldb, M, N, K, tn, ep, s, sk->splits);
+    hipError_t e = dtype ? launch<bf16_t, EPI_PART>(bm, A, lda, B, ldb, M, N, K, tn, ep, s, sk->splits)
+                         : launch<float, EPI_PART>(bm, A, lda, B, ldb, M, N, K, tn, ep, s, sk->splits);
     if (e != hipSuccess || sk->defer) return e;
     return splitk_add(*sk, M, N, X, ldx, s);
   }
-  return dtype ? launch<bf16_t, EPI_RESID>(A, lda, B, ldb, M, N, K, tn, ep, s)
-               : launch<float, EPI_RESID>(A, lda, B, ldb, M, N, K, tn, ep, s);
+  return dtype ? launch<bf16_t, EPI_RESID>(bm, A, lda, B, ldb, M, N, K, tn, ep, s)
+               : launch<float, EPI_RESID>(bm, A, lda, B, ldb, M, N, K, tn, ep, s);
 }
 
 hipError_t gemm_swiglu(int dtype, const void* A, int lda, const void* Wgu, int M, int F, int K, void* out,
@@ -654,7 +677,8 @@ hipError_t gemm_swiglu(int dtype, const void* A, int lda, const void* Wgu, int M
   EpiParams ep{};
   ep.out = out;
   ep.F = F;
-  if (!(sk && sk->splits > 1) && M > 256 && M <= 512 && M > kSmallM) {
+  const int bm = tile_rows(GEMM_KIND_GATEUP, M, 2 * F, K);
+  if (!(sk && sk->splits > 1) && M > 256 && M <= 512 && bm == Big::BM) {
     const int tm = cdiv(F, Mid::BN / 2);
     return dtype ? launch_cfg<bf16_t, EPI_SWIGLU, 0, Mid>(A, lda, Wgu, K, M, 2 * F, K, tm, ep, s, 1)
                  : launch_cfg<float, EPI_SWIGLU, 0, Mid>(A, lda, Wgu, K, M, 2 * F, K, tm, ep, s, 1);
@@ -664,8 +688,8 @@ hipError_t gemm_swiglu(int dtype, const void* A, int lda, const void* Wgu, int M
     if (F % 4) return hipErrorInvalidValue;
     ep.part = sk->part;
     ep.np = tn * kBN;
-    hipError_t e = dtype ? launch<bf16_t, EPI_PART_GU>(A, lda, Wgu, K, M, 2 * F, K, tn, ep, s, sk->splits)
-                         : launch<float, EPI_PART_GU>(A, lda, Wgu, K, M, 2 * F, K, tn, ep, s, sk->splits);
+    hipError_t e = dtype ? launch<bf16_t, EPI_PART_GU>(bm, A, lda, Wgu, K, M, 2 * F, K, tn, ep, s, sk->splits)
+                         : launch<float, EPI_PART_GU>(bm, A, lda, Wgu, K, M, 2 * F, K, tn, ep, s, sk->splits);
     if (e != hipSuccess) return e;
     const dim3 g(cdiv(M * (F / 4), kRedThreads));
     if (dtype)
@@ -676,7 +700,7 @@ hipError_t gemm_swiglu(int dtype, const void* A, int lda, const void* Wgu, int M
                          static_cast<float*>(out));
     return hipGetLastError();
   }
-  if (M > kSmallM) {
+  if (bm == Big::BM) {
     // 256 x 256 tiles, one persistent workgroup per CU
     const int stage_k = dtype ? 2 * TileMma<bf16_t, Big::BM, Big::BN, Big::WM, Big::WN>::kKPerStage
                               : 2 * TileMma<float, Big::BM, Big::BN, Big::WM, Big::WN>::kKPerStage;
@@ -691,8 +715,8 @@ hipError_t gemm_swiglu(int dtype, const void* A, int lda, const void* Wgu, int M
                          static_cast<const float*>(A), lda, static_cast<const float*>(Wgu), M, K, tiles_m, tn, ep);
     return hipGetLastError();
   }
-  return dtype ? launch<bf16_t, EPI_SWIGLU>(A, lda, Wgu, K, M, 2 * F, K, tn, ep, s)
-               : launch<float, EPI_SWIGLU>(A, lda, Wgu, K, M, 2 * F, K, tn, ep, s);
+  return dtype ? launch<bf16_t, EPI_SWIGLU>(bm, A, lda, Wgu, K, M, 2 * F, K, tn, ep, s)
+               : launch<float, EPI_SWIGLU>(bm, A, lda, Wgu, K, M, 2 * F, K, tn, ep, s);
 }
 
 namespace {
@@ -705,7 +729,7 @@ hipError_t qkv_split(const void* A, int lda, const void* Wqkv, int M, int K, con
   const int N = 3 * o.d, tn = cdiv(N, kBN);
   ep.part = sk.part;
   ep.np = tn * kBN;
-  hipError_t e = launch<T, EPI_PART>(A, lda, Wqkv, K, M, N, K, tn, ep, s, sk.splits);
+  hipError_t e = launch<T, EPI_PART>(tile_rows(GEMM_KIND_QKV, M, N, K), A, lda, Wqkv, K, M, N, K, tn, ep, s, sk.splits);
   if (e != hipSuccess) return e;
   const int n_qk = cdiv(M * o.d, kRedThreads), n_v = cdiv(o.d, 64) * cdiv(M, 16);
   if (o.hd == 128)
@@ -727,11 +751,12 @@ hipError_t gemm_qkv(int dtype, const void* A, int lda, const void* Wqkv, int M, 
   ep.qkv = o;
   const int N = 3 * o.d;
   const int tn = cdiv(N, kBN);
+  const int bm = tile_rows(GEMM_KIND_QKV, M, N, K);
   if (o.hd == 128)
-    return dtype ? launch<bf16_t, EPI_QKV, 128>(A, lda, Wqkv, K, M, N, K, tn, ep, s)
-                 : launch<float, EPI_QKV, 128>(A, lda, Wqkv, K, M, N, K, tn, ep, s);
-  return dtype ? launch<bf16_t, EPI_QKV, 64>(A, lda, Wqkv, K, M, N, K, tn, ep, s)
-               : launch<float, EPI_QKV, 64>(A, lda, Wqkv, K, M, N, K, tn, ep, s);
+    return dtype ? launch<bf16_t, EPI_QKV, 128>(bm, A, lda, Wqkv, K, M, N, K, tn, ep, s)
+                 : launch<float, EPI_QKV, 128>(bm, A, lda, Wqkv, K, M, N, K, tn, ep, s);
+  return dtype ? launch<bf16_t, EPI_QKV, 64>(bm, A, lda, Wqkv, K, M, N, K, tn, ep, s)
+               : launch<float, EPI_QKV, 64>(bm, A, lda, Wqkv, K, M, N, K, tn, ep, s);
 }
 
 }  // namespace dllm

@@ -30,8 +30,10 @@ struct SplitK {
   int splits;
   bool defer = false;   // resid: write the partials only; the caller adds them (resid_rmsnorm / splitk_add)
 };
-// parts for M rows, tiles_n 256-wide column tiles (gate/up: F / 128) and K
-int gemm_splits(int M, int tiles_n, int K, int dtype);
+// split-K parts of a projection of M rows, N outputs (gate/up: 2 F, the
+// gate and up rows) and depth K
+enum { GEMM_KIND_QKV = 0, GEMM_KIND_RESID = 1, GEMM_KIND_GATEUP = 2 };
+int gemm_splits(int kind, int M, int N, int K, int dtype);
 size_t gemm_partial_bytes(int M, int tiles_n, int splits);
 
 // X[M][N] (fp32, row stride ldx) += A[M][K] B[N][K]^T

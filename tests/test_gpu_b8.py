@@ -91,8 +91,13 @@ def test_two_layer_8b_width_forward_in_bench_launch_config(P, b8_two_layer):
         return softmax_stats(om.lm_logits(h, wts, shape, scale=1.0), 16)
     ref, ref2 = oracle(w_np), oracle(perturbed(w_np))
     got = {k: v[b * 256 + sample] for k, v in out.numpy().items()}
-    print(compare_stats(got, ref, 2e-2, label="2-layer 8B width", max_exceptions=allowed_flips(ref, ref2),
-                        id_ranks=4), "oracle's own flips", flip_rows(ref, ref2))
+    # individual logits: max(2e-2, 1.25 x the oracle's own spread under a
+    # relative 1e-6 weight perturbation), as for the cached step below;
+    # entropies and log-partition values keep 2e-2
+    spread = max(float(np.max(np.abs(ref.lmax - ref2.lmax))), float(np.max(np.abs(ref.topk_logit - ref2.topk_logit))))
+    rep = compare_stats(got, ref, 2e-2, label="2-layer 8B width", logit_tol=max(2e-2, 1.25 * spread),
+                        max_exceptions=allowed_flips(ref, ref2), id_ranks=4)
+    print(f"oracle noise floor {spread:.3e}, oracle's own flips {flip_rows(ref, ref2)}", rep)
 
 
 def test_batch_invariance(P, b8_two_layer):

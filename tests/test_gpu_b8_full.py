@@ -147,16 +147,20 @@ def test_full_step_base_stats_and_plan(gpu_step):
     plan = orps.select_pivots(ref, res["m_pos"], prm)
     gp = res["plan"]
     gpu_pivots = [gp.pivot_pos[i] for i in range(gp.n_pivots)]
-    compared = excluded = 0
-    for i, pv in enumerate(plan.pivots):
-        if min(pv.feas_margin, pv.rank_margin) > MARGIN:
-            compared += 1
-            assert i < len(gpu_pivots) and gpu_pivots[i] == pv.pos, f"pivot {i}: oracle {pv.pos}, gpu {gpu_pivots}"
-            # the candidates are the pivot's top-4 tokens (r = 0): ranks fixed by the top-k comparison above
-        else:
-            excluded += 1
+    # a pivot whose band-edge and rank margins both exceed 1e-3 must be chosen,
+    # and the chosen ones keep their relative order; a pivot the oracle places
+    # within the margin may be missing, and for each such one the GPU may take
+    # the next row of the ranking instead
+    det = [pv.pos for pv in plan.pivots if min(pv.feas_margin, pv.rank_margin) > MARGIN]
+    undet = [pv.pos for pv in plan.pivots if min(pv.feas_margin, pv.rank_margin) <= MARGIN]
+    missing = [p for p in det if p not in gpu_pivots]
+    assert not missing, f"determined pivots {missing} missing: oracle {[p.pos for p in plan.pivots]}, gpu {gpu_pivots}"
+    assert [p for p in gpu_pivots if p in det] == det, f"order: oracle {det}, gpu {gpu_pivots}"
+    extra = [p for p in gpu_pivots if p not in [pv.pos for pv in plan.pivots]]
+    assert len(extra) <= len(undet), f"gpu pivots {extra} beyond the oracle's {len(undet)} undetermined ones"
+    compared, excluded = len(det), len(undet)
     print(f"plan: oracle pivots {[p.pos for p in plan.pivots]}, gpu {gpu_pivots}; "
-          f"{compared} compared, {excluded} within the 1e-3 margin")
+          f"{compared} determined and chosen, {excluded} within the 1e-3 margin, gpu's others {extra}")
     STATE["plan_report"] = (compared, excluded)
 
 
