@@ -212,12 +212,14 @@ def test_cached_step_two_layer_8b_width(P, b8_two_layer):
     # keys amplify flips of bf16 rounding decisions.  Individual logits (lmax,
     # top-k logits) are held to max(2e-2, 1.25 x spread); entropies and
     # log-partition values keep 2e-2.
-    ref2 = oracle_stats(perturbed(w_np))
-    spread = max(float(np.max(np.abs(ref.lmax - ref2.lmax))),
-                 float(np.max(np.abs(ref.topk_logit - ref2.topk_logit))))
+    # three perturbations (32 rows give few flips each): the largest spread
+    # and flip count set the bounds
+    others = [oracle_stats(perturbed(w_np, seed=46 + i)) for i in range(3)]
+    spread = max(max(float(np.max(np.abs(ref.lmax - o.lmax))), float(np.max(np.abs(ref.topk_logit - o.topk_logit))))
+                 for o in others)
     logit_tol = max(2e-2, 1.25 * spread)
+    own = max(flip_rows(ref, o) for o in others)
     rep = compare_stats(got, ref, 2e-2, label="cached step 2-layer 8B width", logit_tol=logit_tol,
-                        max_exceptions=allowed_flips(ref, ref2), id_ranks=4)
-    print(f"oracle noise floor {spread:.3e}, logit bound {logit_tol:.3e}, oracle's own flips {flip_rows(ref, ref2)}",
-          rep)
+                        max_exceptions=max(2, 2 * own), id_ranks=4)
+    print(f"oracle noise floor {spread:.3e}, logit bound {logit_tol:.3e}, oracle's own flips {own}", rep)
     model_p.close()
