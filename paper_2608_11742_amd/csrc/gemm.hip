@@ -39,6 +39,17 @@ using Quad = GemmCfg<128, 256, 4, 2, 1>;
 using Mid = GemmCfg<256, 192, 4, 2, 2>;
 constexpr int kBN = 256;          // Big and Small: column tile of the split-K partials and the QKV / residual launches
 constexpr int kGroupM = 8;
+#ifndef DLLM_PINGPONG
+#define DLLM_PINGPONG 1
+#endif
+constexpr bool kPingPong = DLLM_PINGPONG;
+
+// mainloop of a tile configuration: bf16 256 x 256 tiles take the two-group
+// schedule (PingPongMma), every other configuration TileMma
+template <typename T, class Cfg, bool TRANS>
+using MainLoop = std::conditional_t<kPingPong && std::is_same_v<T, bf16_t> && Cfg::BM == 256 && Cfg::BN == 256 &&
+                                        Cfg::WM == 4 && Cfg::WN == 2,
+                                    PingPongMma<T, TRANS>, TileMma<T, Cfg::BM, Cfg::BN, Cfg::WM, Cfg::WN, TRANS>>;
 #ifndef DLLM_SMALL_M_MAX
 #define DLLM_SMALL_M_MAX 64
 #endif
@@ -167,7 +178,7 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
                                                                 int K, int tiles_m, int tiles_n, EpiParams ep) {
   constexpr int kBM = Cfg::BM, kWavesN = Cfg::WN;
   constexpr bool kTrans = EPI == EPI_SWIGLU;
-  using TM = TileMma<T, Cfg::BM, Cfg::BN, Cfg::WM, Cfg::WN, kTrans>;
+  using TM = MainLoop<T, Cfg, kTrans>;
   constexpr bool kSplit = EPI == EPI_PART || EPI == EPI_PART_GU;
   __shared__ __attribute__((aligned(16))) uint8_t smem[TM::kSmem];
   int tm, tn, part = 0;
@@ -409,7 +420,7 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
 template <typename T, class Cfg>
 __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_swiglu_persist_kernel(
     const T* __restrict__ A, int lda, const T* __restrict__ B, int M, int K, int tiles_m, int tiles_n, EpiParams ep) {
-  using TM = TileMma<T, Cfg::BM, Cfg::BN, Cfg::WM, Cfg::WN, true>;
+  using TM = MainLoop<T, Cfg, true>;
   __shared__ __attribute__((aligned(16))) uint8_t smem[TM::kSmem];
   const int ntiles = tiles_m * tiles_n;
   const int nk = K / TM::kKPerStage;

@@ -279,6 +279,194 @@ struct TileMma {
   }
 };
 
+// 256 x 256 tile with the waves of TileMma<T, 256, 256, 4, 2> (64 x 128 each,
+// same accumulator layout) run as two groups that take turns on the matrix
+// cores.  Waves 0-3 (group 0: rows 0-127 of the tile) and waves 4-7 (group 1:
+// rows 128-255) put one wave of each group on every SIMD.  Each K sub-step
+// (64 bytes of K) is one phase per group: a load phase (the sub-step's 12
+// fragment reads, copies into the ring, waits) and an MFMA phase (32 MFMAs
+// on registers).  Group 1 runs one phase behind group 0, and a workgroup
+// barrier ends every phase, so that on each SIMD one wave issues MFMAs back
+// to back while the other loads: the LDS reads of one group overlap the
+// other's MFMAs instead of all waves reading at once after a barrier.
+//
+// Ring of two stage slots, as in TileMma.  Copies of stage s + 2 go into the
+// slot of stage s as soon as no wave reads that part any more, split so that
+// every copy has about four phases to land:
+//   A rows 0-127 (read by group 0 only): group 1, in its load phase of
+//     sub-step (s, 1), after group 0's last read of them;
+//   A rows 128-255: group 0, in its load phase of (s + 1, 0);
+//   B: group 1, in its load phase of (s + 1, 0).
+// A group waits for its copies of a stage at the end of the load phase just
+// before the first read of that stage by any wave, so the barrier that ends
+// the phase publishes them.  Past the last stage the copies repeat stage
+// ns - 1 (same data, into parts no wave reads any more), keeping every wait
+// count uniform.
+template <typename T, bool TRANS = false>
+struct PingPongMma {
+  using Base = TileMma<T, 256, 256, 4, 2, TRANS>;
+  static constexpr int kWaves = 8, kThreads = 512;
+  static constexpr int kWTM = Base::kWTM, kWTN = Base::kWTN, kFM = Base::kFM, kFN = Base::kFN;
+  static constexpr int kRowBytes = Base::kRowBytes, kStageA = Base::kStageA, kStage = Base::kStage;
+  static constexpr int kSmem = Base::kSmem;
+  static constexpr int kKPerStage = Base::kKPerStage;
+  static constexpr int kIH = 4;   // copy instructions per wave for half of A (128 rows / 8 / 4 waves)
+  static constexpr int kIB = 8;   // for B (256 rows / 8 / 4 waves)
+  static_assert(kFM == 4 && kFN == 8, "ping-pong layout");
+
+  __device__ __forceinline__ static int swz(int r, int c) { return Base::swz(r, c); }
+
+  // the wave's copies: group 0 copies A rows 128-255, group 1 A rows 0-127 and B
+  struct Loader {
+    uint32_t ga[kIH], gb[kIB];
+    uint32_t lds0;
+    rsrc_t ra, rb;
+    int q, grp;   // index within the group, group
+    template <class AOff, class BOff>
+    __device__ __forceinline__ Loader(uint8_t* smem, const uint8_t* A, const uint8_t* B, AOff a_off, BOff b_off) {
+      const int lane = threadIdx.x & 63;
+      const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
+      q = wave & 3;
+      grp = wave >> 2;
+      const uint32_t chunk_off = uint32_t((lane & 7) ^ (lane >> 3)) << 4;
+      const int a_first = grp ? 0 : 128;
+#pragma unroll
+      for (int i = 0; i < kIH; ++i) ga[i] = a_off(a_first + (q * kIH + i) * 8 + (lane >> 3)) + chunk_off;
+#pragma unroll
+      for (int i = 0; i < kIB; ++i) gb[i] = b_off((q * kIB + i) * 8 + (lane >> 3)) + chunk_off;
+      lds0 = lds_address(smem);
+      ra = buffer_rsrc(A);
+      rb = buffer_rsrc(B);
+    }
+    // this wave's half of A of stage st into ring slot `slot`
+    __device__ __forceinline__ void copy_a(int st, int slot) const {
+      const uint32_t koff = uint32_t(st) * kRowBytes;
+      const uint32_t base = lds0 + slot * kStage + ((grp ? 0 : 16) + q * kIH) * 1024;
+#pragma unroll
+      for (int i = 0; i < kIH; ++i) lds_dma16(ra, ga[i], koff, base + i * 1024);
+    }
+    // this wave's share of B of stage st (group 1 only)
+    __device__ __forceinline__ void copy_b(int st, int slot) const {
+      const uint32_t koff = uint32_t(st) * kRowBytes;
+      const uint32_t base = lds0 + slot * kStage + kStageA + q * kIB * 1024;
+#pragma unroll
+      for (int i = 0; i < kIB; ++i) lds_dma16(rb, gb[i], koff, base + i * 1024);
+    }
+  };
+
+  // Copies of stage `st` (0 or 1) of a tile into ring slot st, as run expects
+  // them when PRE: stage 0 whole (every wave its TileMma share), stage 1 split
+  // by group (group 0: A rows 128-255; group 1: A rows 0-127, then B).
+  template <class AOff, class BOff>
+  __device__ __forceinline__ static void issue_stage(uint8_t* smem, const uint8_t* A, const uint8_t* B, AOff a_off,
+                                                     BOff b_off, int nk, int st) {
+    if (st == 0) {
+      Base::issue_stage(smem, A, B, a_off, b_off, nk, 0);
+    } else {
+      const Loader ld(smem, A, B, a_off, b_off);
+      const int s1 = min(1, (nk >> 1) - 1);
+      ld.copy_a(s1, 1);
+      if (ld.grp) ld.copy_b(s1, 1);
+    }
+  }
+
+  template <bool PRE = false, class AOff, class BOff>
+  __device__ __forceinline__ static void run(uint8_t* smem, const uint8_t* A, const uint8_t* B, AOff a_off,
+                                             BOff b_off, int nk, f32x4 (&acc)[kFM][kFN]) {
+    if constexpr (!PRE) {
+      issue_stage(smem, A, B, a_off, b_off, nk, 0);
+      issue_stage(smem, A, B, a_off, b_off, nk, 1);
+    }
+    const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
+    if (wave >= 4)
+      group_loop<1>(smem, A, B, a_off, b_off, nk, acc);
+    else
+      group_loop<0>(smem, A, B, a_off, b_off, nk, acc);
+    wait_vmcnt<0>();
+    __syncthreads();   // the caller may reuse the LDS
+  }
+
+ private:
+  template <int G, class AOff, class BOff>
+  __device__ __forceinline__ static void group_loop(uint8_t* smem, const uint8_t* A, const uint8_t* B, AOff a_off,
+                                                    BOff b_off, int nk, f32x4 (&acc)[kFM][kFN]) {
+    const int lane = threadIdx.x & 63;
+    const Loader ld(smem, A, B, a_off, b_off);
+    const int wave = int(threadIdx.x) >> 6;
+    const int wm = wave / 2, wn = wave % 2;
+    const int ns = nk >> 1;
+    const int fr = lane & 15, fc = lane >> 4;
+
+#pragma unroll
+    for (int m = 0; m < kFM; ++m)
+#pragma unroll
+      for (int n = 0; n < kFN; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    u32x4 af[2][kFM], bfr[2][kFN];
+    auto reads = [&](int r, int slot, int h) {
+      const uint8_t* st = smem + slot * kStage;
+#pragma unroll
+      for (int m = 0; m < kFM; ++m)
+        af[r][m] = *reinterpret_cast<const u32x4*>(st + swz(wm * kWTM + m * 16 + fr, 4 * h + fc));
+#pragma unroll
+      for (int n = 0; n < kFN; ++n)
+        bfr[r][n] = *reinterpret_cast<const u32x4*>(st + kStageA + swz(wn * kWTN + n * 16 + fr, 4 * h + fc));
+    };
+    auto mfmas = [&](int r) {
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < kFM * kFN; ++i) {
+        if constexpr (TRANS)
+          Mfma<T>::run(acc[i / kFN][i % kFN], bfr[r][i % kFN], af[r][i / kFN]);
+        else
+          Mfma<T>::run(acc[i / kFN][i % kFN], af[r][i / kFN], bfr[r][i % kFN]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    auto phase_end = [&]() {
+      __builtin_amdgcn_sched_barrier(0);
+      barrier_lds();
+      __builtin_amdgcn_sched_barrier(0);
+    };
+
+    // stage 0 landed in every wave (stage 1 may be in flight), then published
+    if constexpr (G == 0)
+      wait_vmcnt<kIH>();
+    else
+      wait_vmcnt<kIH + kIB>();
+    phase_end();
+    if constexpr (G == 1) phase_end();   // one phase behind group 0
+
+    for (int s = 0; s < ns; ++s) {
+      const int slot = s & 1;
+      // load phase of sub-step (s, 0)
+      reads(0, slot, 0);
+      if (s > 0) {
+        const int st = min(s + 1, ns - 1);
+        if constexpr (G == 0)
+          ld.copy_a(st, slot ^ 1);
+        else
+          ld.copy_b(st, slot ^ 1);
+      }
+      if constexpr (G == 0) wait_vmcnt<kIH>();   // A rows 128-255 of stage s landed (stage s + 1's in flight)
+      phase_end();
+      mfmas(0);
+      phase_end();
+      // load phase of sub-step (s, 1)
+      reads(1, slot, 1);
+      if constexpr (G == 1) {
+        wait_lgkmcnt0();
+        ld.copy_a(min(s + 2, ns - 1), slot);
+        wait_vmcnt<kIH>();   // A rows 0-127 and B of stage s + 1 landed
+      }
+      phase_end();
+      mfmas(1);
+      phase_end();
+    }
+    if constexpr (G == 0) phase_end();   // matches group 1's extra phase
+  }
+};
+
 // Map a linear workgroup id to a (tile_m, tile_n) pair.  Workgroups are
 // dispatched round-robin over the 8 XCDs, each with its own L2; the id is
 // first remapped so that every XCD receives a contiguous range, then tiles
