@@ -106,7 +106,9 @@ typedef struct {
 
 /* Cached keys/values of a prefix (the block-wise prefix cache used with RPS
  * in Section 5.3).  k: [n_layers][n_heads][cap][head_dim], post-RoPE;
- * vt: [n_layers][n_heads][head_dim][cap] (values transposed).  Model dtype. */
+ * vt: [n_layers][n_heads][head_dim][cap] (values transposed).  k in the
+ * model dtype; vt float32 for f32 models and IEEE binary16 (values saturated
+ * to +-65504) for bf16 models, the type the attention's P V product uses. */
 typedef struct {
     void* k;
     void* vt;

@@ -9,10 +9,11 @@ softmax attention, SwiGLU feed-forward, untied embedding and LM head, no biases.
 Every operation is its textbook definition written out once; matrix products
 use numpy's matmul in float64.
 
-``mirror=True`` rounds values to bfloat16 (nearest-even) at the points where
-the GPU contract stores bfloat16: the inputs of every projection (normed
-activations, attention output, SwiGLU output), Q/K/V after RoPE and the final
-normed hidden state.  Everything else stays float64.
+``mirror=True`` rounds values at the points where the GPU contract stores
+16-bit values: to bfloat16 (nearest-even) the inputs of every projection
+(normed activations, attention output, SwiGLU output), Q and K after RoPE and
+the final normed hidden state; to IEEE binary16 (nearest-even, saturated to
++-65504) the attention values V.  Everything else stays float64.
 """
 from __future__ import annotations
 
@@ -29,6 +30,16 @@ def bf16_round(x: np.ndarray) -> np.ndarray:
     with np.errstate(over="ignore"):
         r = ((b + half + lsb) >> drop) << drop
     return r.view(np.float64)
+
+
+F16_MAX = 65504.0
+
+
+def f16_round(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to the nearest IEEE binary16 value (ties to even)
+    after saturating them to the finite range +-65504, kept as float64."""
+    x = np.clip(np.asarray(x, dtype=np.float64), -F16_MAX, F16_MAX)
+    return x.astype(np.float16).astype(np.float64)
 
 
 def rmsnorm(x: np.ndarray, eps: float) -> np.ndarray:
@@ -87,6 +98,7 @@ def layer(x, weights, l, shape, pos, mirror=False, prefix_kv=None, collect=None,
     [S, P + S] with a prefix.
     """
     R = bf16_round if mirror else (lambda t: t)
+    RV = f16_round if mirror else (lambda t: t)
     S, d = x.shape
     H, hd = shape.n_heads, shape.head_dim
     a = R(rmsnorm(x, shape.rms_eps))
@@ -96,7 +108,7 @@ def layer(x, weights, l, shape, pos, mirror=False, prefix_kv=None, collect=None,
     v = qkv[:, 2 * d:3 * d].reshape(S, H, hd).transpose(1, 0, 2)
     q = R(rope(q, pos, shape.rope_base))
     k = R(rope(k, pos, shape.rope_base))
-    v = R(v)
+    v = RV(v)
     if collect is not None:
         collect.append((k, v))
     if prefix_kv is not None:

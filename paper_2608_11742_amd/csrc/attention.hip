@@ -15,7 +15,8 @@
 // every lane holds one query's scores for 4 keys per 16-key block: the
 // online-softmax max/sum and the output rescale stay per lane, and the
 // probabilities feed the P V product (computed as O^T = V^T P^T) directly as
-// MFMA operands without an LDS round trip.
+// MFMA operands without an LDS round trip.  bf16 models keep V^T in IEEE
+// binary16 (written so by the QKV projection), and P V runs on fp16 MFMAs.
 #include "kernels.h"
 #include "common.h"
 #include "mainloop.h"
@@ -332,10 +333,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
       }
       // O^T += V^T P^T over keys 32 half .. 32 half + 31
       if constexpr (Elem<T>::per_chunk == 8) {
-        // P enters the product as a pair of bf16 values, hi = bf16(p) and
-        // lo = bf16(p - hi) (both rounded to nearest even), so the weights keep
-        // about 16 significant bits: bf16 weights alone add an error as large as
-        // the bf16 rounding of the output over a thousand keys.
+        // P and V^T in IEEE binary16 (11 significant bits, probabilities
+        // below 2^8 by the lazy reference), one fp16 MFMA per block, where
+        // bf16 weights alone would add an error as large as the bf16 rounding
+        // of the output over a thousand keys.  The split layout (launches
+        // that leave CUs idle, and short blocks over a cached prefix) adds a
+        // second MFMA on lo = fp16(p - hi), about 22 significant bits: it
+        // costs little where the chip is not full.
+        constexpr bool kPairP = kSplit;
         u32x4 pb[NQB], pl[NQB];
 #pragma unroll
         for (int qb = 0; qb < NQB; ++qb)
@@ -343,9 +348,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
           for (int w = 0; w < 4; ++w) {
             const int kk = w >> 1, i0 = 2 * (w & 1);
             const float a0 = p[kk][qb][i0], a1 = p[kk][qb][i0 + 1];
-            const uint32_t hh = pack_bf16x2(a0, a1);
-            pb[qb][w] = hh;
-            pl[qb][w] = pack_bf16x2(a0 - __uint_as_float(hh << 16), a1 - __uint_as_float(hh & 0xffff0000u));
+            pb[qb][w] = pack_f16x2(a0, a1);
+            if constexpr (kPairP)
+              pl[qb][w] = pack_f16x2(a0 - f16_lo(pb[qb][w]), a1 - f16_hi(pb[qb][w]));
           }
 #pragma unroll
         for (int db = 0; db < C::NDB; ++db) {
@@ -353,8 +358,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
           const u32x4 vf = *reinterpret_cast<const u32x4*>(sv + swz(db * 16 + fr, 4 * half + g, C::CV * 16));
 #pragma unroll
           for (int qb = 0; qb < NQB; ++qb) {
-            Mfma<T>::run(o[db][qb], vf, pb[qb]);
-            Mfma<T>::run(o[db][qb], vf, pl[qb]);
+            MfmaF16::run(o[db][qb], vf, pb[qb]);
+            if constexpr (kPairP) MfmaF16::run(o[db][qb], vf, pl[qb]);
           }
         }
       } else {

@@ -53,6 +53,31 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
+// two floats -> two IEEE binary16 values in one word (a in the low half),
+// hardware round to nearest even
+__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
+  typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+  const f16x2_t v = {static_cast<_Float16>(a), static_cast<_Float16>(b)};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// the two binary16 halves of a word as floats (exact)
+__device__ __forceinline__ float f16_lo(uint32_t w) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w & 0xffffu)));
+}
+__device__ __forceinline__ float f16_hi(uint32_t w) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w >> 16)));
+}
+
+// Attention values (V, stored transposed as V^T) of bf16 models are kept as
+// IEEE binary16, saturated to its finite range (+-65504): the P V product
+// then runs on fp16 MFMAs with the probabilities in fp16 (11 significant
+// bits against bf16's 8).
+__device__ __forceinline__ float vt_sat(float v) { return __builtin_amdgcn_fmed3f(v, -65504.0f, 65504.0f); }
+__device__ __forceinline__ uint32_t pack_vt2(float a, float b) { return pack_f16x2(vt_sat(a), vt_sat(b)); }
+__device__ __forceinline__ void store_vt(float* p, float v) { *p = v; }
+__device__ __forceinline__ void store_vt(bf16_t* p, float v) { p->bits = uint16_t(pack_vt2(v, 0.f)); }
+
 // silu(g) = g / (1 + e^-g) with the hardware base-2 exponential and
 // reciprocal (about 1 ulp each)
 __device__ __forceinline__ float silu_fast(float g) {
@@ -71,6 +96,15 @@ __device__ __forceinline__ void store_f(bf16_t* p, float v) { p->bits = f2bf(v);
 //       is the full dot product regardless of the hardware's k order.
 // Output layout of a 16x16 block (both): lane l, element i holds
 // D[4 * (l / 16) + i][l % 16].
+// 16x16 block, 32 k per step, IEEE binary16 operands (8 per lane)
+struct MfmaF16 {
+  __device__ __forceinline__ static void run(f32x4& acc, u32x4 a, u32x4 b) {
+    typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), acc, 0,
+                                                 0, 0);
+  }
+};
+
 template <typename T> struct Mfma;
 template <> struct Mfma<bf16_t> {
   __device__ __forceinline__ static void run(f32x4& acc, u32x4 a, u32x4 b) {

@@ -363,9 +363,10 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
               *reinterpret_cast<const u32x4*>(st + off(r, c16));
         }
       } else {
-        // V^T: a lane's 4 values of a block are 4 consecutive positions of
-        // one head dim, i.e. 8 contiguous bytes of a V^T row: stored straight
-        // from registers (4 rows of one sequence when seq % 4 == 0)
+        // V^T (IEEE binary16, see pack_vt2): a lane's 4 values of a block are
+        // 4 consecutive positions of one head dim, i.e. 8 contiguous bytes of
+        // a V^T row: stored straight from registers (4 rows of one sequence
+        // when seq % 4 == 0)
         uint16_t* vt = reinterpret_cast<uint16_t*>(o.vt);
         const bool vec4 = (o.seq % 4) == 0 && (o.vt_ld % 4) == 0;
 #pragma unroll
@@ -378,11 +379,11 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
             const int cin = cin0 + n * 16 + lc, h = cin / hd, dim = cin % hd;
             if (vec4 && row + 3 < M) {
               *reinterpret_cast<u32x2*>(vt + (size_t(b * o.H + h) * hd + dim) * o.vt_ld + sp) =
-                  u32x2{pack_bf16x2(acc[m][n][0], acc[m][n][1]), pack_bf16x2(acc[m][n][2], acc[m][n][3])};
+                  u32x2{pack_vt2(acc[m][n][0], acc[m][n][1]), pack_vt2(acc[m][n][2], acc[m][n][3])};
             } else {
               for (int i = 0; i < 4 && row + i < M; ++i) {
                 const int bi = (row + i) / o.seq, si = (row + i) - bi * o.seq;
-                vt[(size_t(bi * o.H + h) * hd + dim) * o.vt_ld + si] = uint16_t(pack_bf16x2(acc[m][n][i], 0.f));
+                vt[(size_t(bi * o.H + h) * hd + dim) * o.vt_ld + si] = uint16_t(pack_vt2(acc[m][n][i], 0.f));
               }
             }
           }
@@ -615,7 +616,7 @@ __device__ __forceinline__ void splitk_v(const float* __restrict__ part, int spl
     const int idx = threadIdx.x + kRedThreads * e, c = idx >> 4, r = idx & 15, row = r0 + r, col = c0 + c;
     if (row >= M || col >= d) continue;
     const int b = row / o.seq, sp = row - b * o.seq, h = col / o.hd, dim = col - h * o.hd;
-    store_f(static_cast<T*>(o.vt) + (size_t(b * o.H + h) * o.hd + dim) * o.vt_ld + sp, tile[r][c]);
+    store_vt(static_cast<T*>(o.vt) + (size_t(b * o.H + h) * o.hd + dim) * o.vt_ld + sp, tile[r][c]);
   }
 }
 

@@ -59,11 +59,15 @@ class Model:
         return self._reserve(B.dllm_workspace_bytes_packed(self.handle, shared_len, block_len, n_branch, n_lm_pos))
 
     def new_kv_cache(self, cap: int):
-        """Device buffers for a prefix cache of `cap` positions (cap rounded up to 8)."""
+        """Device buffers for a prefix cache of `cap` positions (cap rounded up to 8).
+
+        Keys in the model's dtype; values (transposed) in IEEE float16 for
+        bf16 models, float32 for fp32 models."""
         cap = (cap + 7) // 8 * 8
         s = self.shape
         k = torch.empty(s.n_layers, s.n_heads, cap, s.head_dim, dtype=self.torch_dtype, device=self.device)
-        vt = torch.empty(s.n_layers, s.n_heads, s.head_dim, cap, dtype=self.torch_dtype, device=self.device)
+        v_dtype = torch.float16 if self.torch_dtype == torch.bfloat16 else self.torch_dtype
+        vt = torch.empty(s.n_layers, s.n_heads, s.head_dim, cap, dtype=v_dtype, device=self.device)
         return k, vt, cap
 
     def forward(self, tokens, lm_pos, out: B.Stats | None = None, n_lm_pos: int | None = None, row_scale=None,

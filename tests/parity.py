@@ -85,7 +85,10 @@ def flip_rows(ref, other, margin: float = MARGIN, id_ranks: int = 4) -> int:
     perturbed weights) changes a decision that `ref` fixes by more than
     `margin`: the argmax or one of the first id_ranks top-k ids.  This is the
     number of flips the oracle's own rounding noise produces, the yardstick for
-    a bf16 implementation's."""
+    a bf16 implementation's.  `other` may be a list of such evaluations: the
+    largest count among them."""
+    if isinstance(other, (list, tuple)):
+        return max(flip_rows(ref, o, margin, id_ranks) for o in other)
     am = (ref.argmax_margin > margin) & (other.argmax != ref.argmax)
     K = ref.topk_id.shape[1]
     ki = min(id_ranks, K)
@@ -112,9 +115,17 @@ def perturbed(weights: dict, rel: float = 1e-6, seed: int = 46) -> dict:
     return out
 
 
+def perturbations(weights: dict, n: int = 3, rel: float = 1e-6) -> list:
+    """n perturbed copies of the weights (seeds 46, 47, ...): the flip count of
+    one random perturbation is itself noisy, the largest of a few is the
+    yardstick."""
+    return [perturbed(weights, rel=rel, seed=46 + i) for i in range(n)]
+
+
 def allowed_flips(ref, other, floor: int = 2, factor: float = 2.0, **kw) -> int:
     """Exceptions allowed to a bf16 implementation: `factor` times the flips of
-    the oracle's own perturbed evaluation, at least `floor`."""
+    the oracle's own perturbed evaluation(s) (the largest, for a list), at
+    least `floor`."""
     return max(floor, int(np.ceil(factor * flip_rows(ref, other, **kw))))
 
 

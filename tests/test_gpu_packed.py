@@ -12,7 +12,7 @@ from oracle import model as om
 from oracle import rps as orps
 from oracle.decode import rps_decode as oracle_decode, model_forward, model_packed_lookahead
 from oracle.stats import softmax_stats
-from tests.parity import compare_stats, perturbed, allowed_flips, flip_rows, MARGIN
+from tests.parity import compare_stats, perturbed, perturbations, allowed_flips, flip_rows, MARGIN
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -108,9 +108,9 @@ def test_packed_forward_small_bf16_against_mirror(P, small_bf16, S, b0, B, n):
     out = model.forward_packed(torch.from_numpy(packed).to(DEV), S, b0, B, n, torch.from_numpy(lm_pos).to(DEV),
                                scale=3.0)
     torch.cuda.synchronize()
-    ref, ref2 = [softmax_stats(om.packed_logits(packed, w, shape, S, b0, B, n, lm_pos, scale=3.0,
+    ref, *ref2 = [softmax_stats(om.packed_logits(packed, w, shape, S, b0, B, n, lm_pos, scale=3.0,
                                                 mirror=True).reshape(-1, shape.vocab), 16)
-                 for w in (w_np, perturbed(w_np))]
+                 for w in (w_np, *perturbations(w_np))]
     print(compare_stats(out.numpy(), ref, 2e-2, max_exceptions=allowed_flips(ref, ref2), id_ranks=4,
                         label=f"packed bf16 S{S} B{B} n{n}"), "oracle's own flips", flip_rows(ref, ref2))
 

@@ -11,7 +11,7 @@ from synth import ModelShape
 from oracle import model as om
 from oracle import rps as orps
 from oracle.stats import softmax_stats
-from tests.parity import compare_stats, MARGIN, perturbed, allowed_flips, flip_rows
+from tests.parity import compare_stats, MARGIN, perturbed, perturbations, allowed_flips, flip_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -113,8 +113,8 @@ def test_forward_small_bf16_against_mirror(P, small_bf16):
     lm_pos = np.arange(64, 136, dtype=np.int32)
     out = model.forward(torch.from_numpy(toks).to(DEV), torch.from_numpy(lm_pos).to(DEV), scale=3.0)
     torch.cuda.synchronize()
-    ref, ref2 = [softmax_stats(om.forward_logits(toks, w, shape, lm_pos, scale=3.0, mirror=True).reshape(
-        -1, shape.vocab), 16) for w in (w_np, perturbed(w_np))]
+    ref, *ref2 = [softmax_stats(om.forward_logits(toks, w, shape, lm_pos, scale=3.0, mirror=True).reshape(
+        -1, shape.vocab), 16) for w in (w_np, *perturbations(w_np))]
     print(compare_stats(out.numpy(), ref, 2e-2, max_exceptions=allowed_flips(ref, ref2), id_ranks=4,
                         label="forward small bf16"), "oracle's own flips", flip_rows(ref, ref2))
 
@@ -173,10 +173,10 @@ def test_forward_small_bf16_many_sequences(P, small_bf16):
     out = model.forward(torch.from_numpy(toks).to(DEV), torch.from_numpy(lm_pos).to(DEV), scale=3.0)
     torch.cuda.synchronize()
     got = out.numpy()
-    wp = perturbed(w_np)
+    wps = perturbations(w_np)
     for b in (5, 62):
-        ref, ref2 = [softmax_stats(om.forward_logits(toks[b:b + 1], w, shape, lm_pos, scale=3.0,
-                                                     mirror=True).reshape(-1, shape.vocab), 16) for w in (w_np, wp)]
+        ref, *ref2 = [softmax_stats(om.forward_logits(toks[b:b + 1], w, shape, lm_pos, scale=3.0,
+                                                      mirror=True).reshape(-1, shape.vocab), 16) for w in (w_np, *wps)]
         sl = slice(b * len(lm_pos), (b + 1) * len(lm_pos))
         print(compare_stats({k: v[sl] for k, v in got.items()}, ref, 2e-2, max_exceptions=allowed_flips(ref, ref2),
                             id_ranks=4, label=f"64 x 200 bf16 seq {b}"), "oracle's own flips", flip_rows(ref, ref2))
@@ -194,8 +194,8 @@ def test_forward_small_bf16_few_rows(P, small_bf16, S):
     lm_pos = np.arange(S // 2, S, dtype=np.int32)
     out = model.forward(torch.from_numpy(toks).to(DEV)[None], torch.from_numpy(lm_pos).to(DEV), scale=3.0)
     torch.cuda.synchronize()
-    ref, ref2 = [softmax_stats(om.forward_logits(toks[None], w, shape, lm_pos, scale=3.0, mirror=True).reshape(
-        -1, shape.vocab), 16) for w in (w_np, perturbed(w_np))]
+    ref, *ref2 = [softmax_stats(om.forward_logits(toks[None], w, shape, lm_pos, scale=3.0, mirror=True).reshape(
+        -1, shape.vocab), 16) for w in (w_np, *perturbations(w_np))]
     print(compare_stats(out.numpy(), ref, 2e-2, max_exceptions=allowed_flips(ref, ref2), id_ranks=4,
                         label=f"forward small bf16 1x{S}"), "oracle's own flips", flip_rows(ref, ref2))
 
@@ -256,7 +256,7 @@ def test_cached_prefix_forward_small_bf16(P, small_bf16, Pn, Bk):
             h = om.hidden(blocks[b], w, shape, pos_offset=Pn, mirror=True, prefix_kv=kv)
             refs.append(om.lm_logits(h, w, shape, scale=3.0))
         return softmax_stats(np.concatenate(refs), 16)
-    ref, ref2 = oracle(w_np), oracle(perturbed(w_np))
+    ref, ref2 = oracle(w_np), [oracle(w) for w in perturbations(w_np)]
     print(compare_stats(out.numpy(), ref, 2e-2, max_exceptions=allowed_flips(ref, ref2), id_ranks=4,
                         label=f"cached bf16 prefix {Pn} block {Bk}"), "oracle's own flips", flip_rows(ref, ref2))
 

@@ -81,6 +81,23 @@ def test_bf16_round_matches_torch_on_float32_values():
     assert om.bf16_round(np.array([1.0 + 3 * 2 ** -8]))[0] == 1.0 + 2 ** -6
 
 
+def test_f16_round_matches_torch_and_saturates():
+    """The mirror's binary16 rounding of attention values: torch's float16
+    conversion (round to nearest even) on values inside the finite range,
+    including subnormals, and saturation to +-65504 beyond it."""
+    x = np.concatenate([synth.weight_np(6, "r", (10000,), std=10.0, dtype="f32"),
+                        synth.weight_np(7, "r", (2000,), std=1e-5, dtype="f32")]).astype(np.float64)
+    ours = om.f16_round(x)
+    theirs = torch.from_numpy(x).to(torch.float16).to(torch.float64).numpy()
+    assert np.array_equal(ours, theirs)
+    # ties go to even: 1 + 2^-11 lies halfway between 1 and 1 + 2^-10
+    assert om.f16_round(np.array([1.0 + 2 ** -11]))[0] == 1.0
+    assert om.f16_round(np.array([1.0 + 3 * 2 ** -11]))[0] == 1.0 + 2 ** -9
+    # smallest subnormal, and beyond the finite range
+    assert om.f16_round(np.array([2.0 ** -24]))[0] == 2.0 ** -24
+    assert list(om.f16_round(np.array([65504.0, 70000.0, -1e9]))) == [65504.0, 65504.0, -65504.0]
+
+
 def test_degenerate_weights_reduce_to_embedding_lookup():
     w = _weights(SMALL)
     for l in range(SMALL.n_layers):
