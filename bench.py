@@ -376,6 +376,14 @@ def main():
             kern[name]["tflops"] = round(lf[name] / (kern[name]["ms_per_launch"] * 1e-3) / 1e12, 1)
     dom_ms, dom_n = prof_dom[dom]
     achieved = lf[dom] / (dom_ms / dom_n * 1e-3) / 1e12
+    # the device's own register-only MFMA rate (best of three), outside the
+    # timed region: with random operands at every instruction it is the
+    # attainable ceiling under the power limit, below the published peak
+    ceiling = {"random_operands": round(max(P.dllm_mfma_ceiling(True) for _ in range(3)), 1),
+               "constant_operands": round(max(P.dllm_mfma_ceiling(False) for _ in range(3)), 1),
+               "unit": "TFLOP/s"}
+    ceiling["frac_of_random_operand_ceiling"] = round(achieved / ceiling["random_operands"], 4)
+    log(f"MFMA ceiling: {ceiling}")
     total_flops = step_flops(shape, wl.capacity, wl.seq, wl.capacity * n0)
     res = {
         "metric": METRIC,
@@ -405,6 +413,7 @@ def main():
             "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": recorded_traffic(),
             "flop_per_launch": lf[dom], "ms_per_launch": round(dom_ms / dom_n, 4), "launches_timed": dom_n,
+            "mfma_ceiling_measured": ceiling,
         },
         "kernels": kern,
         "kernels_note": "per-class times from two more steps with every launch bracketed by events, "

@@ -259,6 +259,16 @@ dllm_status dllm_profile_begin(dllm_model* m, int32_t max_launches);
  * brackets only the kernel it reports on.  class_mask == 0 is EINVAL. */
 dllm_status dllm_profile_begin_classes(dllm_model* m, int32_t max_launches, uint32_t class_mask);
 dllm_status dllm_profile_end(dllm_model* m, float* ms, int32_t* launches);
+/* Benchmark calibration, not part of the method: the bf16 MFMA rate this
+ * device sustains on a register-only loop of v_mfma_f32_16x16x32_bf16 (no
+ * memory traffic), in TFLOP/s, written to *tflops (host memory).  With
+ * random_operands != 0 every MFMA takes different random bf16 operands, as a
+ * GEMM on real data does: the datapath then draws more power and the
+ * sustained clock drops, so this is the attainable ceiling against which a
+ * GEMM's rate is judged (the published 2.5 PFLOP/s assumes the peak clock).
+ * Runs about 25 ms of work on `stream` and waits for it; creates and destroys
+ * two events. */
+dllm_status dllm_mfma_ceiling(int32_t random_operands, float* tflops, dllm_stream stream);
 
 /* ---------------------------------------------------------------- scheduler */
 

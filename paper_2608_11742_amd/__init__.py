@@ -11,7 +11,7 @@ from .binding import (  # noqa: F401
     vocab_entropy_topk, vocab_entropy_topk_noalloc, vocab_entropy_topk_workspace_bytes, rps_select_pivots, rps_build_branches, rps_build_packed,
     dllm_workspace_bytes_packed,
     rps_lookahead_score, rps_commit, sched_commit, params, new_plan, new_decision, read_plan, read_decision, lib,
-    dllm_profile_begin, dllm_profile_end,
+    dllm_profile_begin, dllm_profile_end, dllm_mfma_ceiling,
 )
 from .model import Model  # noqa: F401
 from .step import RpsStep, rps_decode, baseline_decode  # noqa: F401

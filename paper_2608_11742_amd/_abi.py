@@ -89,6 +89,7 @@ SIGNATURES = {
     "dllm_profile_begin": (i32, [vp, i32]),
     "dllm_profile_begin_classes": (i32, [vp, i32, C.c_uint32]),
     "dllm_profile_end": (i32, [vp, C.POINTER(f32), C.POINTER(i32)]),
+    "dllm_mfma_ceiling": (i32, [i32, C.POINTER(f32), vp]),
     "rps_select_pivots": (i32, [C.POINTER(StatsC), vp, i32, C.POINTER(RpsParams), vp, vp]),
     "rps_build_branches": (i32, [vp, i32, vp, i32, i32, vp, vp]),
     "rps_build_packed": (i32, [vp, i32, vp, i32, i32, i32, vp, vp]),

@@ -153,6 +153,14 @@ def dllm_profile_end(handle) -> dict:
     return {name: (float(ms[i]), int(n[i])) for i, name in enumerate(_abi.PROF_NAMES)}
 
 
+def dllm_mfma_ceiling(random_operands: bool = True, stream=None) -> float:
+    """Sustained bf16 MFMA rate of the device on a register-only loop, TFLOP/s
+    (random_operands: different random operands at every instruction)."""
+    out = C.c_float(0.0)
+    _check(lib().dllm_mfma_ceiling(1 if random_operands else 0, C.byref(out), _stream(stream)))
+    return float(out.value)
+
+
 def dllm_workspace_bytes(handle, batch: int, seq: int, n_lm_pos: int) -> int:
     return lib().dllm_workspace_bytes(handle, batch, seq, n_lm_pos)
 

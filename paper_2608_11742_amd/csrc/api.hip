@@ -264,6 +264,34 @@ dllm_status dllm_profile_end(dllm_model* m, float* ms, int32_t* launches) {
   return DLLM_OK;
 }
 
+dllm_status dllm_mfma_ceiling(int32_t random_operands, float* tflops, dllm_stream stream) {
+  if (!tflops) return fail(DLLM_EINVAL, "dllm_mfma_ceiling: NULL tflops");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int dev = 0, cus = 0;
+  TRY_HIP(hipGetDevice(&dev), "hipGetDevice");
+  TRY_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev), "hipDeviceGetAttribute");
+  const int wg = 2 * std::max(cus, 1);
+  double flop = 0.0;
+  TRY_HIP(dllm::mfma_calibration(random_operands != 0, 2000, wg, &flop, s), "mfma_calibration (warm-up)");
+  hipEvent_t e0, e1;
+  TRY_HIP(hipEventCreate(&e0), "hipEventCreate");
+  if (hipEventCreate(&e1) != hipSuccess) {
+    (void)hipEventDestroy(e0);
+    return fail(DLLM_EHIP, "hipEventCreate");
+  }
+  float ms = 0.f;
+  hipError_t e = hipEventRecord(e0, s);
+  if (e == hipSuccess) e = dllm::mfma_calibration(random_operands != 0, 20000, wg, &flop, s);
+  if (e == hipSuccess) e = hipEventRecord(e1, s);
+  if (e == hipSuccess) e = hipEventSynchronize(e1);
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  TRY_HIP(e, "mfma_calibration");
+  *tflops = ms > 0.f ? float(flop / (double(ms) * 1e-3) / 1e12) : 0.f;
+  return DLLM_OK;
+}
+
 size_t dllm_workspace_bytes(const dllm_model* m, int32_t batch, int32_t seq, int32_t n_lm_pos) {
   if (!m || batch < 1 || seq < 1 || n_lm_pos < 1) return 0;
   return plan_forward(m->desc, batch, seq, batch * n_lm_pos).total;

@@ -125,4 +125,7 @@ hipError_t rps_commit_step(int32_t* tokens, int seq, int32_t* m_pos, int n_m, co
 hipError_t sched_commit_step(int32_t* tokens, int seq, int32_t* m_pos, int n_m, const StatsOut& st, int rule, int k,
                             int32_t* n_m_out, int32_t* committed, int32_t* n_committed, hipStream_t s);
 
+// register-only bf16 MFMA loop (benchmark calibration); *flop: the launch's MFMA work
+hipError_t mfma_calibration(bool random_operands, int iters, int workgroups, double* flop, hipStream_t s);
+
 }  // namespace dllm

@@ -14,6 +14,7 @@
 //   lse = M + log S, H = log S - T / S, lmax = M,
 // and a 64-way merge of the sorted partial top-16 lists.
 #include <algorithm>
+#include <type_traits>
 
 #include "kernels.h"
 #include "mainloop.h"
@@ -34,9 +35,13 @@ constexpr float kLog2e = 1.4426950408889634f, kLn2 = 0.6931471805599453f;
 // tile) when there are more than 128 rows, else 128 (8 waves of 64 x 64).
 // kSegs scan threads per row, each scanning 64 logits per pass; a pass
 // stages kSegs * 64 columns of the fp32 logit tile in LDS.
+// The MFMA blocks are computed transposed (TRANS), so that a lane holds 4
+// consecutive logits of one row and stages them with one 16-byte LDS write;
+// bf16 256-row tiles take the two-group mainloop of the projections.
 template <typename T, int BM>
 struct LmCfg {
-  using TM = TileMma<T, BM, kCols, BM == 256 ? 4 : 2, BM == 256 ? 2 : 4>;
+  using TM = std::conditional_t<BM == 256 && std::is_same_v<T, bf16_t>, PingPongMma<T, true>,
+                                TileMma<T, BM, kCols, BM == 256 ? 4 : 2, BM == 256 ? 2 : 4, true>>;
   static constexpr int kSegs = kThreads / BM;
   static constexpr int kPassCols = kSegs * kSegCols;
   static constexpr int kPasses = kCols / kPassCols;
@@ -184,13 +189,12 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_kernel(const T* __restrict
 #pragma unroll
       for (int mi = 0; mi < TM::kFM; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < TM::kFN; ++ni)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int r = wm * TM::kWTM + mi * 16 + 4 * (lane >> 4) + i;
-            const int c = wn * TM::kWTN + ni * 16 + (lane & 15) - pass * Cfg::kPassCols;
-            *reinterpret_cast<float*>(smem + r * kRowStride + (c >> 6) * kSegStride + (c & 63) * 4) = acc[mi][ni][i];
-          }
+        for (int ni = 0; ni < TM::kFN; ++ni) {
+          // (transposed blocks) row 16 mi + lane % 16, columns 16 ni + 4 (lane / 16) + 0..3
+          const int r = wm * TM::kWTM + mi * 16 + (lane & 15);
+          const int c = wn * TM::kWTN + ni * 16 + 4 * (lane >> 4) - pass * Cfg::kPassCols;
+          *reinterpret_cast<f32x4*>(smem + r * kRowStride + (c >> 6) * kSegStride + (c & 63) * 4) = acc[mi][ni];
+        }
     }
     __syncthreads();
     // scan 64 logits of row srow: running statistics, and a bit mask of the

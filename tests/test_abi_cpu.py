@@ -165,3 +165,9 @@ def test_model_create_without_device_reports_hip_error(abi):
     h = C.c_void_p()
     assert lib.dllm_model_create(C.byref(_desc(_abi)), C.byref(w), C.byref(h)) == 5
     assert "hipMalloc" in _err(lib)
+
+
+def test_mfma_ceiling_rejects_null_output(abi):
+    _abi, lib = abi
+    assert lib.dllm_mfma_ceiling(1, None, None) == 1   # DLLM_EINVAL, before any device call
+    assert "NULL" in _err(lib)
