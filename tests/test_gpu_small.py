@@ -491,3 +491,13 @@ def test_profile_begin_classes_brackets_only_the_chosen_classes(P, tiny):
     assert all(n == 0 for name, (_, n) in prof.items() if name != "attention")
     with pytest.raises(Bd.DllmError):
         Bd._check(Bd.lib().dllm_profile_begin_classes(model.handle, 10, 0))
+
+
+def test_mfma_ceiling_calibration(P):
+    """The benchmark's register-only MFMA calibration: constant operands run
+    near the published 2.5 PFLOP/s, random operands lower (power-limited
+    clock), both finite and below the published peak."""
+    const = max(P.dllm_mfma_ceiling(False) for _ in range(2))
+    rand = max(P.dllm_mfma_ceiling(True) for _ in range(2))
+    print(f"\nMFMA ceiling: constant operands {const:.0f} TFLOP/s, random operands {rand:.0f} TFLOP/s")
+    assert 1000.0 < rand <= const < 2600.0
