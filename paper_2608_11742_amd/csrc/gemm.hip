@@ -22,9 +22,14 @@ namespace {
 // Big 256 x 256 with 8 waves (two per SIMD, one workgroup per CU); Small
 // 64 x 256 with 2 waves for GEMMs of at most kSmallM rows, where a 256-row
 // tile would mostly multiply clamped duplicate rows (two workgroups per CU).
-template <int BM_, int BN_, int WM_, int WN_, int MIN_BLOCKS>
+// EARLY: the TileMma schedule that hands a consumed ring slot to its next
+// copies half a stage sooner (measured faster where the weights stream from
+// HBM at one tile per CU: 4-10% on the Quad and Mid launches, no change on
+// Small).
+template <int BM_, int BN_, int WM_, int WN_, int MIN_BLOCKS, bool EARLY = false>
 struct GemmCfg {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, kThreads = WM_ * WN_ * 64, kMinBlocks = MIN_BLOCKS;
+  static constexpr bool kEarly = EARLY;
 };
 using Big = GemmCfg<256, 256, 4, 2, 2>;
 using Small = GemmCfg<64, 256, 1, 2, 2>;
@@ -32,11 +37,11 @@ using Small = GemmCfg<64, 256, 1, 2, 2>;
 // 128 x 256 tiles of 8 waves of 32 x 128 (two per SIMD, as Big), so that a
 // 65-256-row projection wastes fewer clamped rows and needs half the split-K
 // parts of 256-row tiles
-using Quad = GemmCfg<128, 256, 4, 2, 1>;
+using Quad = GemmCfg<128, 256, 4, 2, 1, true>;
 // gate/up with 257-512 rows: 256 x 192 tiles (waves of 64 x 96, 48 gate + 48
 // up rows each) give 2 x F / 96 = 256 workgroups for the 8B shape, one per CU,
 // where 256 x 256 tiles leave a quarter of the CUs idle
-using Mid = GemmCfg<256, 192, 4, 2, 2>;
+using Mid = GemmCfg<256, 192, 4, 2, 2, true>;
 constexpr int kBN = 256;          // Big and Small: column tile of the split-K partials and the QKV / residual launches
 constexpr int kGroupM = 8;
 #ifndef DLLM_PINGPONG
@@ -47,9 +52,10 @@ constexpr bool kPingPong = DLLM_PINGPONG;
 // mainloop of a tile configuration: bf16 256 x 256 tiles take the two-group
 // schedule (PingPongMma), every other configuration TileMma
 template <typename T, class Cfg, bool TRANS>
-using MainLoop = std::conditional_t<kPingPong && std::is_same_v<T, bf16_t> && Cfg::BM == 256 && Cfg::BN == 256 &&
-                                        Cfg::WM == 4 && Cfg::WN == 2,
-                                    PingPongMma<T, TRANS>, TileMma<T, Cfg::BM, Cfg::BN, Cfg::WM, Cfg::WN, TRANS>>;
+using MainLoop =
+    std::conditional_t<kPingPong && std::is_same_v<T, bf16_t> && Cfg::BM == 256 && Cfg::BN == 256 && Cfg::WM == 4 &&
+                           Cfg::WN == 2,
+                       PingPongMma<T, TRANS>, TileMma<T, Cfg::BM, Cfg::BN, Cfg::WM, Cfg::WN, TRANS, Cfg::kEarly>>;
 #ifndef DLLM_SMALL_M_MAX
 #define DLLM_SMALL_M_MAX 64
 #endif
@@ -548,75 +554,104 @@ __global__ __launch_bounds__(kRedThreads) void splitk_swiglu_kernel(const float*
 }
 
 
-// Q and K: one thread per (row, q or k, head, dim < HD/2) pair; sums the two
-// partners, rotates them and writes both to the head-major layout
+// four consecutive values stored at once (p 8-byte aligned for bf16, 16 for fp32)
+__device__ __forceinline__ void store4(bf16_t* p, f32x4 v) {
+  *reinterpret_cast<u32x2*>(p) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+}
+__device__ __forceinline__ void store4(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
+__device__ __forceinline__ void store4_vt(bf16_t* p, f32x4 v) {
+  *reinterpret_cast<u32x2*>(p) = u32x2{pack_vt2(v[0], v[1]), pack_vt2(v[2], v[3])};
+}
+__device__ __forceinline__ void store4_vt(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
+
+// Q and K: one thread per (row, q or k, head, 4 dims < HD/2): sums the two
+// partner groups over the parts in order, rotates them and writes both to
+// the head-major layout, 16-byte partial loads and 4-value stores
 template <typename T, int HD>
 __device__ __forceinline__ void splitk_qk(const float* __restrict__ part, int splits, int M, int np,
                                           const QkvOut& o, int blk) {
-  constexpr int half = HD / 2;
-  const int d = o.d;
+  constexpr int half = HD / 2, q4 = half / 4;
+  const int d = o.d, per_row = d / 4;   // (q, k) x heads x half / 4
   const int i = blk * kRedThreads + threadIdx.x;
-  if (i >= M * d) return;
-  const int row = i / d, p = i - row * d;
-  const int which = p / (d / 2), rest = p - which * (d / 2);
-  const int h = rest / half, dim = rest - h * half;
-  const int c1 = which * d + h * HD + dim;
-  float x1 = 0.f, x2 = 0.f;
-  const float* src = part + size_t(row) * np + c1;
+  if (i >= M * per_row) return;
+  const int row = i / per_row, p = i - row * per_row;
+  const int which = p / (per_row / 2), rest = p - which * (per_row / 2);
+  const int h = rest / q4, dim = (rest - h * q4) * 4;
+  const float* src = part + size_t(row) * np + which * d + h * HD + dim;
   const size_t stride = size_t(M) * np;
+  f32x4 x1 = f32x4{0.f, 0.f, 0.f, 0.f}, x2 = x1;
   int s = 0;
   for (; s + 2 <= splits; s += 2) {
-    const float a0 = src[s * stride], b0 = src[s * stride + half], a1 = src[(s + 1) * stride],
-                b1 = src[(s + 1) * stride + half];
+    const f32x4 a0 = *reinterpret_cast<const f32x4*>(src + s * stride),
+                b0 = *reinterpret_cast<const f32x4*>(src + s * stride + half),
+                a1 = *reinterpret_cast<const f32x4*>(src + (s + 1) * stride),
+                b1 = *reinterpret_cast<const f32x4*>(src + (s + 1) * stride + half);
     x1 += a0;
     x2 += b0;
     x1 += a1;
     x2 += b1;
   }
   for (; s < splits; ++s) {
-    x1 += src[s * stride];
-    x2 += src[s * stride + half];
+    x1 += *reinterpret_cast<const f32x4*>(src + s * stride);
+    x2 += *reinterpret_cast<const f32x4*>(src + s * stride + half);
   }
-  const float2 cs = o.rope[size_t(qkv_pos(o, row)) * half + dim];
+  const float4* cs4 = reinterpret_cast<const float4*>(o.rope + size_t(qkv_pos(o, row)) * half + dim);
+  const float4 c01 = cs4[0], c23 = cs4[1];   // (cos, sin) of dims dim .. dim + 3
+  const float cs_c[4] = {c01.x, c01.z, c23.x, c23.z}, cs_s[4] = {c01.y, c01.w, c23.y, c23.w};
+  f32x4 y1, y2;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    y1[e] = x1[e] * cs_c[e] - x2[e] * cs_s[e];
+    y2[e] = x1[e] * cs_s[e] + x2[e] * cs_c[e];
+  }
   const int b = row / o.seq, sp = row - b * o.seq;
-  T* dst = static_cast<T*>(which == 0 ? o.q : o.k) + (size_t(b * o.H + h) * o.seq + sp) * HD;
-  store_f(dst + dim, x1 * cs.x - x2 * cs.y);
-  store_f(dst + dim + half, x1 * cs.y + x2 * cs.x);
+  T* dst = static_cast<T*>(which == 0 ? o.q : o.k) + (size_t(b * o.H + h) * o.seq + sp) * HD + dim;
+  store4(dst, y1);
+  store4(dst + half, y2);
 }
 
 // V: 16-row x 64-column tiles transposed through LDS so that both the partial
-// reads (along columns) and the V^T writes (along positions) are contiguous
+// reads (16 bytes along a row) and the V^T writes (4 positions of one head
+// dim) are contiguous
 template <typename T>
 __device__ __forceinline__ void splitk_v(const float* __restrict__ part, int splits, int M, int np, const QkvOut& o,
                                          int bx, int by, float (&tile)[16][65]) {
   const int c0 = bx * 64, r0 = by * 16, d = o.d;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int idx = threadIdx.x + kRedThreads * e, r = idx >> 6, c = idx & 63, row = r0 + r, col = c0 + c;
-    float v = 0.f;
-    if (row < M && col < d) {
+  {
+    const int r = threadIdx.x >> 4, c = (threadIdx.x & 15) * 4, row = r0 + r, col = c0 + c;
+    f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (row < M && col < d) {   // d % 4 == 0: the 4 columns are in range together
       const float* src = part + size_t(row) * np + 2 * d + col;
       const size_t stride = size_t(M) * np;
       int p = 0;
       for (; p + 4 <= splits; p += 4) {
-        const float a0 = src[p * stride], a1 = src[(p + 1) * stride], a2 = src[(p + 2) * stride],
-                    a3 = src[(p + 3) * stride];
+        const f32x4 a0 = *reinterpret_cast<const f32x4*>(src + p * stride),
+                    a1 = *reinterpret_cast<const f32x4*>(src + (p + 1) * stride),
+                    a2 = *reinterpret_cast<const f32x4*>(src + (p + 2) * stride),
+                    a3 = *reinterpret_cast<const f32x4*>(src + (p + 3) * stride);
         v += a0;
         v += a1;
         v += a2;
         v += a3;
       }
-      for (; p < splits; ++p) v += src[p * stride];
+      for (; p < splits; ++p) v += *reinterpret_cast<const f32x4*>(src + p * stride);
     }
-    tile[r][c] = v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) tile[r][c + e] = v[e];
   }
   __syncthreads();
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int idx = threadIdx.x + kRedThreads * e, c = idx >> 4, r = idx & 15, row = r0 + r, col = c0 + c;
-    if (row >= M || col >= d) continue;
-    const int b = row / o.seq, sp = row - b * o.seq, h = col / o.hd, dim = col - h * o.hd;
-    store_vt(static_cast<T*>(o.vt) + (size_t(b * o.H + h) * o.hd + dim) * o.vt_ld + sp, tile[r][c]);
+  const int c = threadIdx.x >> 2, rg = (threadIdx.x & 3) * 4, col = c0 + c, row = r0 + rg;
+  if (col >= d || row >= M) return;
+  const int b = row / o.seq, sp = row - b * o.seq, h = col / o.hd, dim = col - h * o.hd;
+  T* dst = static_cast<T*>(o.vt) + (size_t(b * o.H + h) * o.hd + dim) * o.vt_ld + sp;
+  // 4 positions of one sequence, aligned
+  if ((o.seq % 4) == 0 && row + 3 < M && (reinterpret_cast<uintptr_t>(dst) & (4 * sizeof(T) - 1)) == 0) {
+    store4_vt(dst, f32x4{tile[rg][c], tile[rg + 1][c], tile[rg + 2][c], tile[rg + 3][c]});
+  } else {
+    for (int e = 0; e < 4 && row + e < M; ++e) {
+      const int bi = (row + e) / o.seq, si = (row + e) - bi * o.seq;
+      store_vt(static_cast<T*>(o.vt) + (size_t(bi * o.H + h) * o.hd + dim) * o.vt_ld + si, tile[rg + e][c]);
+    }
   }
 }
 
@@ -736,6 +771,7 @@ namespace {
 template <typename T>
 hipError_t qkv_split(const void* A, int lda, const void* Wqkv, int M, int K, const QkvOut& o, hipStream_t s,
                      const SplitK& sk) {
+  if (o.d % 8) return hipErrorInvalidValue;   // the reduction takes groups of 4 dims of every head half
   EpiParams ep{};
   ep.qkv = o;
   const int N = 3 * o.d, tn = cdiv(N, kBN);
@@ -743,7 +779,7 @@ hipError_t qkv_split(const void* A, int lda, const void* Wqkv, int M, int K, con
   ep.np = tn * kBN;
   hipError_t e = launch<T, EPI_PART>(tile_rows(GEMM_KIND_QKV, M, N, K), A, lda, Wqkv, K, M, N, K, tn, ep, s, sk.splits);
   if (e != hipSuccess) return e;
-  const int n_qk = cdiv(M * o.d, kRedThreads), n_v = cdiv(o.d, 64) * cdiv(M, 16);
+  const int n_qk = cdiv(M * (o.d / 4), kRedThreads), n_v = cdiv(o.d, 64) * cdiv(M, 16);
   if (o.hd == 128)
     hipLaunchKernelGGL((splitk_qkv_kernel<T, 128>), dim3(n_qk + n_v), dim3(kRedThreads), 0, s, sk.part, sk.splits,
                        M, ep.np, o, n_qk);

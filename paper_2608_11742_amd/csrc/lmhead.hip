@@ -37,11 +37,13 @@ constexpr float kLog2e = 1.4426950408889634f, kLn2 = 0.6931471805599453f;
 // stages kSegs * 64 columns of the fp32 logit tile in LDS.
 // The MFMA blocks are computed transposed (TRANS), so that a lane holds 4
 // consecutive logits of one row and stages them with one 16-byte LDS write;
-// bf16 256-row tiles take the two-group mainloop of the projections.
+// bf16 256-row tiles take the two-group mainloop of the projections;
+// 128-row tiles (few rows: the vocabulary streams from HBM) the early-release
+// TileMma schedule.
 template <typename T, int BM>
 struct LmCfg {
   using TM = std::conditional_t<BM == 256 && std::is_same_v<T, bf16_t>, PingPongMma<T, true>,
-                                TileMma<T, BM, kCols, BM == 256 ? 4 : 2, BM == 256 ? 2 : 4, true>>;
+                                TileMma<T, BM, kCols, BM == 256 ? 4 : 2, BM == 256 ? 2 : 4, true, BM == 128>>;
   static constexpr int kSegs = kThreads / BM;
   static constexpr int kPassCols = kSegs * kSegCols;
   static constexpr int kPasses = kCols / kPassCols;

@@ -86,7 +86,14 @@ __device__ __forceinline__ uint32_t lds_address(const void* p) {
 // row 16 m + l % 16 and the 4 consecutive columns 16 n + 4 (l / 16) + i of
 // block (m, n) (instead of 4 consecutive rows of one column): row-contiguous
 // epilogues then store 4 values per lane.
-template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, bool TRANS = false>
+//
+// EARLY: two barriers per stage instead of one.  The first follows sub-step
+// 0, once every wave has read its last fragments of the stage, and hands the
+// slot to the copies of stage j + 2 at once; the second, later in sub-step 1,
+// publishes stage j + 1.  A copy then has about 1.2-1.3 stages of MFMA work to
+// land instead of 0.65-1.0, for launches whose operands stream from HBM with
+// too few bytes in flight per CU to cover its latency.
+template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, bool TRANS = false, bool EARLY = false>
 struct TileMma {
   static constexpr int kWaves = WAVES_M * WAVES_N;
   static constexpr int kThreads = kWaves * kWave;
@@ -251,6 +258,41 @@ struct TileMma {
         read_into(1, cur, 1, decltype(jj)::value);
         __builtin_amdgcn_sched_barrier(0);
       });
+      const uint32_t koff = uint32_t(min(j + 2, ns - 1)) * kRowBytes, sbase = ld.lds0 + cur * kStage;
+      if constexpr (EARLY) {
+        // slot cur is free once every wave's reads of (j, 1) are done
+        barrier_lds();
+        __builtin_amdgcn_sched_barrier(0);
+        // the copies of stage j + 2, one per MFMA of sub-step 1, then MFMAs up
+        // to the point that leaves one MFMA per fragment read of (j + 1, 0)
+        constexpr int kL = kIA + kIB;
+        constexpr int kB2 = kL > kMma - kReads ? kL : kMma - kReads;
+        static_for<0, kB2>([&](auto cc) {
+          constexpr int c = decltype(cc)::value;
+          if constexpr (c < kMma) {
+            mma_one(1, c);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          if constexpr (c < kIA)
+            dma_a(c, koff, sbase);
+          else if constexpr (c < kL)
+            dma_b(c - kIA, koff, sbase);
+          __builtin_amdgcn_sched_barrier(0);
+        });
+        wait_vmcnt<kL>();   // stage j + 1 landed; stage j + 2 may still be in flight
+        barrier_lds();
+        __builtin_amdgcn_sched_barrier(0);
+        static_for<0, (kMma - kB2 > kReads ? kMma - kB2 : kReads)>([&](auto cc) {
+          constexpr int c = decltype(cc)::value;
+          if constexpr (kB2 + c < kMma) {
+            mma_one(1, kB2 + c);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          if constexpr (c < kReads) read_into(0, nxt, 0, c);
+          __builtin_amdgcn_sched_barrier(0);
+        });
+        continue;
+      }
       static_for<0, kPre1>([&](auto ii) {
         mma_one(1, decltype(ii)::value);
         __builtin_amdgcn_sched_barrier(0);
@@ -258,7 +300,6 @@ struct TileMma {
       wait_vmcnt<0>();
       __syncthreads();
       __builtin_amdgcn_sched_barrier(0);
-      const uint32_t koff = uint32_t(min(j + 2, ns - 1)) * kRowBytes, sbase = ld.lds0 + cur * kStage;
       static_for<0, (kMma - kPre1 > kComp1 ? kMma - kPre1 : kComp1)>([&](auto cc) {
         constexpr int c = decltype(cc)::value;
         if constexpr (kPre1 + c < kMma) {
