@@ -63,10 +63,17 @@ constexpr int kSmallM = DLLM_SMALL_M_MAX;
 
 // Row tile of a projection of M rows: Small up to kSmallM rows; Quad where it
 // measured faster than Big (the d-wide O projection up to 512 rows, the
-// F-deep down projection up to 192, QKV and gate/up up to 128); Big above.
+// F-deep down projection at 1, 2 or 4 row tiles up to 512 rows, QKV and
+// gate/up up to 128); Big above.
 int tile_rows(int kind, int M, int N, int K) {
   if (M <= kSmallM) return Small::BM;
-  const int quad_max = kind == GEMM_KIND_RESID ? (K <= N ? 512 : 192) : 128;
+  if (kind == GEMM_KIND_RESID && K > N && M <= 512) {
+    // the F-deep down projection: 128-row tiles when their split-K parts fill
+    // the CUs exactly (1, 2 or 4 row tiles), else 256-row tiles
+    const int tm = cdiv(M, Quad::BM);
+    return (tm & (tm - 1)) == 0 ? Quad::BM : Big::BM;
+  }
+  const int quad_max = kind == GEMM_KIND_RESID ? 512 : 128;
   return M <= quad_max ? Quad::BM : Big::BM;
 }
 
