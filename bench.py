@@ -41,8 +41,8 @@ METRIC = "denoising steps/sec and committed tokens/sec, 8B-shape, lookahead batc
 # the same counter reads for a plain device copy of known size (the
 # --copy-calibration mode).  Valid only for the kernel sources they were
 # measured on: bench.py reports null once those files change.
-TRAFFIC_GATEUP = {"fetch_bytes": 2416523091, "write_bytes": 201456128,
-                  "sources_sha256": "19736712508f6c2bebf7d66182164b8e86920cf2c3ad66a9a651916840215f0e"}
+TRAFFIC_GATEUP = {"fetch_bytes": 2416672693, "write_bytes": 201469747,
+                  "sources_sha256": "f63285d4227dd4bcf740ae6e243f7c1e137d56195401d6127e101986b5604cd8"}
 TRAFFIC_SOURCES = ("paper_2608_11742_amd/csrc/gemm.hip", "paper_2608_11742_amd/csrc/mainloop.h",
                    "paper_2608_11742_amd/csrc/common.h")
 
@@ -155,6 +155,20 @@ def timed(fn, n):
     return (time.perf_counter() - t0) / n
 
 
+def class_breakdown(P, model, fn, n=2):
+    """Per-kernel-class times of n more calls of fn with every launch bracketed
+    by events (outside any timed region), per call: launches, microseconds
+    per launch and milliseconds in total; split-K reductions count with their
+    projection."""
+    P.dllm_profile_begin(model.handle, 600 * (n + 1))
+    for _ in range(n):
+        fn()
+    torch.cuda.synchronize()
+    prof = P.dllm_profile_end(model.handle)
+    return {k: {"launches": c // n, "us_per_launch": round(ms / c * 1e3, 2), "ms": round(ms / n, 3)}
+            for k, (ms, c) in prof.items() if c}
+
+
 def cached_step(P, model, shape, n):
     """KV-cached RPS step: 1024 cached prefix positions, 16 branch blocks of 32."""
     from paper_2608_11742_amd._abi import KvCache
@@ -185,6 +199,8 @@ def cached_step(P, model, shape, n):
     stp.run()
     stp = fresh()
     t = timed(stp.run, n)
+    stp = fresh()
+    kern = class_breakdown(P, model, stp.run)
     rows = wl.capacity * wl.block
     fl = shape.n_layers * (sum(linear_flops(shape, rows).values())
                            + 4.0 * rows * (wl.prompt_len + wl.block) * shape.d_model) \
@@ -192,9 +208,24 @@ def cached_step(P, model, shape, n):
     kv_gb = 2.0 * 2 * shape.n_layers * shape.n_heads * wl.prompt_len * shape.head_dim / 1e9
     out[wl.name] = {"steps_per_s": round(1.0 / t, 2), "ms": round(t * 1e3, 3), "tflops": round(fl / t / 1e12, 1),
                     "gbs": round((weights_gb + kv_gb) / t, 1),
-                    "algorithmic_gb": round(weights_gb + kv_gb, 2), "tflop": round(fl / 1e12, 2)}
+                    "algorithmic_gb": round(weights_gb + kv_gb, 2), "tflop": round(fl / 1e12, 2),
+                    "kernels_per_step": kern}
     log(f"{wl.name}: {t * 1e3:.2f} ms")
     return out
+
+
+def forward_512(P, model, shape, n):
+    """One 512-token denoising forward (statistics on its 256 masked rows)."""
+    dev = torch.device("cuda:0")
+    wl = W.WORKLOADS["b8_forward_bf16"]
+    tokens, m_pos, base = build_state(P, model, wl, dev)
+    fwd = lambda: model.forward(tokens[None], m_pos, out=base)  # noqa: E731
+    t = timed(fwd, n)
+    fl = step_flops(shape, 1, wl.seq, wl.gen_len)
+    log(f"{wl.name}: {t * 1e3:.2f} ms")
+    return {wl.name: {"forwards_per_s": round(1.0 / t, 2), "ms": round(t * 1e3, 3),
+                      "tflops": round(fl / t / 1e12, 1), "tflop": round(fl / 1e12, 2),
+                      "kernels_per_forward": class_breakdown(P, model, fwd)}}
 
 
 def other_configs(P, model, shape, n):
@@ -202,15 +233,7 @@ def other_configs(P, model, shape, n):
     dev = torch.device("cuda:0")
     out = {}
 
-    # single denoising forward, 1 x 512, statistics on the 256 masked rows
-    wl = W.WORKLOADS["b8_forward_bf16"]
-    tokens, m_pos, base = build_state(P, model, wl, dev)
-    t = timed(lambda: model.forward(tokens[None], m_pos, out=base), n)
-    fl = step_flops(shape, 1, wl.seq, wl.gen_len)
-    out[wl.name] = {"forwards_per_s": round(1.0 / t, 2), "ms": round(t * 1e3, 3),
-                    "tflops": round(fl / t / 1e12, 1), "tflop": round(fl / 1e12, 2)}
-    log(f"{wl.name}: {t * 1e3:.2f} ms")
-
+    out.update(forward_512(P, model, shape, n))
     out.update(cached_step(P, model, shape, n))
 
     # full blockwise decode of 256 tokens (Algorithm 1)
@@ -290,6 +313,9 @@ def main():
                     help="skip the other 8B configurations (single forward, cached step, full decode)")
     ap.add_argument("--cached-only", action="store_true",
                     help="only run the KV-cached RPS step --steps times and print its figures (profiling runs)")
+    ap.add_argument("--few-row", action="store_true",
+                    help="only run the 512-token forward and the KV-cached RPS step --steps times each and "
+                         "print their figures with per-class kernel times (profiling runs)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain copy of MIB mebibytes (scale for rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -318,8 +344,10 @@ def main():
         f"({shape.n_params() / 1e9:.2f} B params)")
     max_pos = max(x.seq for x in W.WORKLOADS.values() if x.model == W.WORKLOADS["b8_rps_step_bf16"].model)
     model = P.Model(shape, w, dtype="bf16", max_pos=max_pos)
-    if args.cached_only:
-        print(json.dumps(cached_step(P, model, shape, args.steps)), flush=True)
+    if args.cached_only or args.few_row:
+        res = forward_512(P, model, shape, args.steps) if args.few_row else {}
+        res.update(cached_step(P, model, shape, args.steps))
+        print(json.dumps(res), flush=True)
         model.close()
         return
     tokens, m_pos, base = build_state(P, model, wl, dev)
