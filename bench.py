@@ -211,6 +211,23 @@ def cached_step(P, model, shape, n):
                     "algorithmic_gb": round(weights_gb + kv_gb, 2), "tflop": round(fl / 1e12, 2),
                     "kernels_per_step": kern}
     log(f"{wl.name}: {t * 1e3:.2f} ms")
+    # its HBM-bound sub-case: the batch-1 forward of one 32-position block over
+    # the same cached prefix (the anchor; the cached decodes' block forwards),
+    # statistics on the block's 32 rows
+    block.copy_(snap[0])   # the steps above committed into the block
+    bpos.copy_(snap[1])
+    anchor = lambda: model.forward(block[None], bpos, pos_offset=wl.prompt_len, kv_prefix=kv, out=bbase)  # noqa: E731
+    anchor()
+    ta = timed(anchor, n)
+    fla = shape.n_layers * (sum(linear_flops(shape, wl.block).values())
+                            + 4.0 * wl.block * (wl.prompt_len + wl.block) * shape.d_model) \
+        + 2.0 * wl.block * shape.d_model * shape.vocab
+    out[wl.name]["anchor_forward_1x32"] = {
+        "ms": round(ta * 1e3, 3), "gbs": round((weights_gb + kv_gb) / ta, 1),
+        "frac_of_hbm_peak": round((weights_gb + kv_gb) / ta / PEAK_HBM_GBS, 4),
+        "algorithmic_gb": round(weights_gb + kv_gb, 2), "tflop": round(fla / 1e12, 3),
+        "kernels_per_forward": class_breakdown(P, model, anchor)}
+    log(f"{wl.name} anchor forward 1 x {wl.block}: {ta * 1e3:.2f} ms")
     return out
 
 
