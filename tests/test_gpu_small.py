@@ -184,11 +184,10 @@ def test_forward_small_bf16_many_sequences(P, small_bf16):
 
 @pytest.mark.parametrize("S", [9, 17, 32, 40, 64, 150])
 def test_forward_small_bf16_few_rows(P, small_bf16, S):
-    """Few-row forwards against the mirror oracle: at most 32 rows, the
-    skinny weight-streaming partials (one and two 16-row blocks, ragged);
-    40 and 64 rows, the 64-row GEMM tiles; every split-K reduction of a block
-    forward; at 150 rows, attention in the 32-query layout that a launch with
-    fewer 128-query workgroups than CUs takes."""
+    """Few-row forwards against the mirror oracle: up to 64 rows (ragged: 9,
+    17, 40), the 64-row GEMM tiles with clamped rows and every split-K
+    reduction of a block forward; at 150 rows, attention in the 32-query
+    layout that a launch with fewer 128-query workgroups than CUs takes."""
     shape, w_np, model = small_bf16
     toks = synth.tokens_np(15 + S, "toks", S, shape.vocab - 1)
     toks[S // 2:] = shape.mask_id
