@@ -79,6 +79,34 @@ def copy_calibration(mib):
     print(json.dumps({"copy_bytes_per_launch": n, "launches": 3}), flush=True)
 
 
+def blas_reference(n=20):
+    """hipBLASLt (torch F.linear, bf16 in and out) on the four projection shapes
+    of the 16 x 512 step: a plain GEMM without the library's fused epilogues,
+    as a reference point for its mainloop.  Four rotating weight copies."""
+    import torch.nn.functional as F
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    M, d, f = 8192, 4096, 12288
+    out = {}
+    for name, K, N in (("qkv", d, 3 * d), ("o", d, d), ("gateup", d, 2 * f), ("down", f, d)):
+        x = (torch.randn(M, K, device=dev, generator=g) * 0.5).to(torch.bfloat16)
+        ws = [(torch.randn(N, K, device=dev, generator=g) * 0.02).to(torch.bfloat16) for _ in range(4)]
+        for i in range(3):
+            F.linear(x, ws[i])
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(n):
+            F.linear(x, ws[i % 4])
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / n
+        out[name] = {"us": round(ms * 1e3, 1), "tflops": round(2.0 * M * N * K / ms / 1e9, 1)}
+        del x, ws
+    return out
+
+
 def build_state(P, model, wl, dev):
     shape = wl.model
     prompt = synth.tokens_torch(W.SEED_PROMPT, "prompt", wl.prompt_len, shape.vocab - 1, device=dev)
@@ -333,6 +361,8 @@ def main():
     ap.add_argument("--few-row", action="store_true",
                     help="only run the 512-token forward and the KV-cached RPS step --steps times each and "
                          "print their figures with per-class kernel times (profiling runs)")
+    ap.add_argument("--blas-reference", action="store_true",
+                    help="only time torch F.linear (hipBLASLt) on the step's projection shapes and print them")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain copy of MIB mebibytes (scale for rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -345,6 +375,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.blas_reference:
+        print(json.dumps({"blas_reference": blas_reference()}), flush=True)
         return
     import paper_2608_11742_amd as P
 
