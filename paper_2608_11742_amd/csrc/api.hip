@@ -92,7 +92,7 @@ dllm_status check_stats(const dllm_stats* s, const char* name) {
 
 // Workspace layout of one forward (256-byte aligned regions).
 struct FwdLayout {
-  size_t x, a, q, k, vt, f, hl, lm, lmsrc, part, total;
+  size_t x, a, q, k, vt, f, hl, lm, lmsrc, part, attn, total;
   int vt_ld;
 };
 
@@ -144,6 +144,8 @@ FwdLayout plan_forward(const dllm_model_desc& d, int batch, int seq, int R) {
   L.lm = take(lmhead_workspace(R, d.vocab));
   L.lmsrc = take(size_t(R) * 8);
   L.part = take(plan_gemms(d, int(M)).bytes);
+  const size_t attn_bytes = attn_partial_bytes(batch, d.n_heads, seq, d.head_dim);
+  L.attn = attn_bytes ? take(attn_bytes) : 0;
   L.total = off;
   return L;
 }
@@ -431,6 +433,7 @@ dllm_status forward_impl(dllm_model* m, const int32_t* tokens, int32_t batch, in
       aa.p_cap = kv_prefix->cap;
     }
     aa.o = a;
+    if (L.attn) aa.kv_part = reinterpret_cast<float*>(base + L.attn);
     if (pk) {
       aa.pack_S = pk->S;
       aa.pack_b0 = pk->b0;

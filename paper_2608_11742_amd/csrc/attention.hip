@@ -8,15 +8,21 @@
 // whose 128-query workgroups would leave CUs idle (a single sequence of
 // 512), take 32 queries per workgroup instead: wave w owns the 16 queries of
 // block w % 2 and the keys of half w / 2 of every tile, and the two halves'
-// softmax states are merged at the end.  Keys stream through a
-// two-slot LDS ring in tiles of 64 (K rows and V^T columns), copied from
-// global memory straight into LDS with buffer_load ... lds one tile ahead.
+// softmax states are merged at the end; when even that layout leaves most
+// CUs idle (one block of 32 over a long cached prefix: 32 workgroups), each
+// sequence's key tiles are also split into ranges, one workgroup each, and a
+// merge kernel combines the ranges' states in a fixed order.  Keys stream
+// through a two-slot LDS ring in tiles of 64 (K rows and V^T columns), copied
+// from global memory straight into LDS with buffer_load ... lds one tile
+// ahead.
 // Scores are computed transposed, S^T = K Q^T, so in the MFMA output layout
 // every lane holds one query's scores for 4 keys per 16-key block: the
 // online-softmax max/sum and the output rescale stay per lane, and the
 // probabilities feed the P V product (computed as O^T = V^T P^T) directly as
 // MFMA operands without an LDS round trip.  bf16 models keep V^T in IEEE
 // binary16 (written so by the QKV projection), and P V runs on fp16 MFMAs.
+#include <algorithm>
+
 #include "kernels.h"
 #include "common.h"
 #include "mainloop.h"
@@ -32,6 +38,22 @@ constexpr int kQT = kWaves * kQW;   // queries per workgroup
 constexpr int kKT = 64;             // keys per tile
 constexpr int kSplitMaxQ = 64;      // sequences of at most this many queries take the split layout
 constexpr int kSplitMaxWg = 256;    // so do launches whose 128-query layout has fewer workgroups than this
+// Key split of the split layout: launches of fewer than kKvMinWg workgroups
+// split every sequence's key tiles into up to kKvMaxSplits ranges of at least
+// two tiles (one-tile ranges measured slower: each range pays its own fill
+// and the merge grows), one workgroup each, whose partial states a merge
+// kernel combines
+constexpr int kKvMinWg = 128;
+constexpr int kKvMaxSplits = 16;
+constexpr int kKvTargetWg = 512;
+// floats per partial record: HD output values, m, l, padding to 16 bytes
+constexpr int kv_rec(int hd) { return hd + 4; }
+
+// key ranges of a split-layout launch of wg workgroups over n_tiles key tiles
+int kv_splits_of(int wg, int n_tiles) {
+  if (wg >= kKvMinWg) return 1;
+  return std::max(1, std::min({kKvMaxSplits, n_tiles / 2, kKvTargetWg / wg}));
+}
 
 template <typename T, int HD>
 struct AttnCfg {
@@ -85,8 +107,11 @@ __device__ __forceinline__ int kswz(int r) {
     return r & 7;
 }
 
+// kv_splits > 1 (split layout only): blockIdx.x = query block * kv_splits +
+// key range; the workgroup writes its unnormalised output and (m, l) to
+// a.kv_part instead of the normalised output
 template <typename T, int HD, bool kPacked, bool kSplit>
-__global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_scale_log2) {
+__global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_scale_log2, int kv_splits) {
   using C = AttnCfg<T, HD>;
   static_assert(!(kPacked && kSplit), "the split layout serves unpacked sequences");
   constexpr int NQB = kSplit ? 1 : 2;   // 16-query blocks per wave
@@ -98,7 +123,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
   const int b = blockIdx.z, h = blockIdx.y;
   // split: the wave's query block and key half
   const int qsel = kSplit ? (wave & 1) : 0, hsel = kSplit ? (wave >> 1) : 0;
-  const int q0 = kSplit ? int(blockIdx.x) * kQW + 16 * qsel : int(blockIdx.x) * kQT + wave * kQW;
+  const int qblk = kSplit ? int(blockIdx.x) / kv_splits : int(blockIdx.x);
+  const int q0 = kSplit ? qblk * kQW + 16 * qsel : qblk * kQT + wave * kQW;
   const size_t bh = size_t(b) * a.H + h;
 
   const T* Q = static_cast<const T*>(a.q) + bh * a.Sq * HD;
@@ -127,6 +153,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
     }
   }
   const int n_tiles = n_pt + n_ot + n_bt;
+  // this workgroup's key tiles tb .. te - 1 (a key range of the split layout)
+  int tb = 0, te = n_tiles;
+  if constexpr (kSplit) {
+    const int ks = int(blockIdx.x) % kv_splits;
+    tb = ks * n_tiles / kv_splits;
+    te = (ks + 1) * n_tiles / kv_splits;
+  }
   // branch of each of this lane's two query columns (-1: a shared row)
   int qbr[2];
 #pragma unroll
@@ -228,17 +261,18 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
     lrun[qb] = 0.f;
   }
 
-  issue(0, 0);
+  issue(tb, 0);
   wait_vmcnt<0>();
   __syncthreads();
-  if (ragged(0)) {
-    zero_tail(0, 0);
+  if (ragged(tb)) {
+    zero_tail(tb, 0);
     __syncthreads();
   }
-  for (int t = 0; t < n_tiles; ++t) {
-    const bool more = t + 1 < n_tiles;
-    if (more) issue(t + 1, (t + 1) & 1);   // that slot was last read before the previous barrier
-    const uint8_t* s = smem + (t & 1) * C::STAGE;
+  for (int t = tb; t < te; ++t) {
+    const bool more = t + 1 < te;
+    const int slot = (t - tb) & 1;
+    if (more) issue(t + 1, slot ^ 1);   // that slot was last read before the previous barrier
+    const uint8_t* s = smem + slot * C::STAGE;
     const uint8_t* sv = s + C::KB;
     const Src sr = src(t);
     const int k0 = sr.k0, nk = sr.nk;
@@ -384,7 +418,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
     wait_vmcnt<0>();
     __syncthreads();
     if (more && ragged(t + 1)) {
-      zero_tail(t + 1, (t + 1) & 1);
+      zero_tail(t + 1, slot ^ 1);
       __syncthreads();
     }
   }
@@ -416,6 +450,25 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
 #pragma unroll
       for (int i = 0; i < 4; ++i) o[db][0][i] = o[db][0][i] * sa + xs[(4 * db + i) * 64] * sb;
     lrun[0] = lrun[0] * sa + lb * sb;
+    mrun[0] = m;
+    if (kv_splits > 1) {
+      // the key range's state: unnormalised output rows (this lane: dims
+      // 16 db + 4 g + i of query q), the reference m (log2 units) and l
+      const int q = q0 + fr;
+      const float l = group4_sum(lrun[0]);
+      if (q < a.Sq) {
+        const int ks = int(blockIdx.x) % kv_splits;
+        float* rec = a.kv_part + ((size_t(ks) * a.B * a.H + bh) * a.Sq + q) * kv_rec(HD);
+#pragma unroll
+        for (int db = 0; db < C::NDB; ++db)
+          *reinterpret_cast<f32x4*>(rec + db * 16 + 4 * g) = o[db][0];
+        if (g == 0) {
+          rec[HD] = m;
+          rec[HD + 1] = l;
+        }
+      }
+      return;
+    }
   }
 
   // normalise and store O[b * Sq + q][h * HD + dim]
@@ -433,6 +486,25 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a, float qk_
   }
 }
 
+// merge of the key ranges' partial states: out[b * Sq + q][h * HD + dim] =
+// sum_s o_s 2^(m_s - m) / sum_s l_s 2^(m_s - m), m = max_s m_s, the ranges
+// added in order; one workgroup of HD threads per (b, h, q)
+template <typename T, int HD>
+__global__ __launch_bounds__(HD) void attn_merge_kernel(AttnArgs a, int kv_splits) {
+  const int q = blockIdx.x, h = blockIdx.y, b = blockIdx.z, dim = threadIdx.x;
+  const size_t bh = size_t(b) * a.H + h, stride = size_t(a.B) * a.H * a.Sq * kv_rec(HD);
+  const float* rec = a.kv_part + (bh * a.Sq + q) * kv_rec(HD);
+  float m = -INFINITY;
+  for (int ks = 0; ks < kv_splits; ++ks) m = fmaxf(m, rec[ks * stride + HD]);
+  float o = 0.f, l = 0.f;
+  for (int ks = 0; ks < kv_splits; ++ks) {
+    const float w = __builtin_amdgcn_exp2f(rec[ks * stride + HD] - m);
+    o += rec[ks * stride + dim] * w;
+    l += rec[ks * stride + HD + 1] * w;
+  }
+  store_f(static_cast<T*>(a.o) + (size_t(b) * a.Sq + q) * (size_t(a.H) * HD) + size_t(h) * HD + dim, o / l);
+}
+
 template <typename T, int HD>
 hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
   // the V^T copies read whole 16-byte chunks inside each row of pitch vt_ld / p_cap
@@ -441,19 +513,31 @@ hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
                        a.pack_b0 < 0 || a.pack_b0 + a.pack_B > a.pack_S))
     return hipErrorInvalidValue;
   const float scale = 1.4426950408889634f / sqrtf(float(HD));
-  if (a.pack_B > 0)
+  if (a.pack_B > 0) {
     hipLaunchKernelGGL((attn_kernel<T, HD, true, false>), dim3(cdiv(a.Sq, kQT), a.H, a.B), dim3(kThreads), 0, s, a,
-                       scale);
-  else if (a.Sq <= kSplitMaxQ || cdiv(a.Sq, kQT) * a.H * a.B < kSplitMaxWg)
-    hipLaunchKernelGGL((attn_kernel<T, HD, false, true>), dim3(cdiv(a.Sq, kQW), a.H, a.B), dim3(kThreads), 0, s, a,
-                       scale);
-  else
+                       scale, 1);
+  } else if (a.Sq <= kSplitMaxQ || cdiv(a.Sq, kQT) * a.H * a.B < kSplitMaxWg) {
+    const int wg = cdiv(a.Sq, kQW) * a.H * a.B;
+    const int n_tiles = (a.kp ? cdiv(a.p_len, kKT) : 0) + cdiv(a.Sq, kKT);
+    const int kv = a.kv_part ? kv_splits_of(wg, n_tiles) : 1;
+    hipLaunchKernelGGL((attn_kernel<T, HD, false, true>), dim3(cdiv(a.Sq, kQW) * kv, a.H, a.B), dim3(kThreads), 0,
+                       s, a, scale, kv);
+    if (kv > 1) hipLaunchKernelGGL((attn_merge_kernel<T, HD>), dim3(a.Sq, a.H, a.B), dim3(HD), 0, s, a, kv);
+  } else {
     hipLaunchKernelGGL((attn_kernel<T, HD, false, false>), dim3(cdiv(a.Sq, kQT), a.H, a.B), dim3(kThreads), 0, s, a,
-                       scale);
+                       scale, 1);
+  }
   return hipGetLastError();
 }
 
 }  // namespace
+
+size_t attn_partial_bytes(int B, int H, int Sq, int hd) {
+  // the split layout with few workgroups; at most kKvMaxSplits key ranges
+  const bool split = Sq <= kSplitMaxQ || cdiv(Sq, kQT) * H * B < kSplitMaxWg;
+  if (!split || cdiv(Sq, kQW) * H * B >= kKvMinWg) return 0;
+  return size_t(kKvMaxSplits) * B * H * Sq * kv_rec(hd) * sizeof(float);
+}
 
 hipError_t attention(int dtype, const AttnArgs& a, hipStream_t s) {
   if (dtype) return a.hd == 128 ? launch_attn<bf16_t, 128>(a, s) : launch_attn<bf16_t, 64>(a, s);

@@ -74,8 +74,14 @@ struct AttnArgs {
   // pack_b0 .. pack_b0+pack_B-1; a cached prefix stays visible to every row;
   // pack_B == 0: no packing
   int pack_S = 0, pack_b0 = 0, pack_B = 0;
+  // split layout with few workgroups: the keys are split over workgroups whose
+  // partial softmax states are merged afterwards; workspace of
+  // attn_partial_bytes (nullable: no key split)
+  float* kv_part = nullptr;
 };
 hipError_t attention(int dtype, const AttnArgs& a, hipStream_t s);
+// workspace for the key split of an attention over B x H x Sq queries (0: never split)
+size_t attn_partial_bytes(int B, int H, int Sq, int hd);
 
 // LM-head rows of a packed lookahead forward: (1 + n_branch) * n_lm rows, the
 // shared sequence's then each branch's; row[] is the packed row each reads,

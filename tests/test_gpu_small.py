@@ -228,12 +228,44 @@ def test_cached_prefix_forward_tiny(P, tiny):
     print(compare_stats(out.numpy(), ref, 1e-4, label="cached forward"))
 
 
-@pytest.mark.parametrize("Pn,Bk", [(20, 1), (20, 32), (100, 17), (130, 64), (64, 33)])
+@pytest.mark.parametrize("Pn,Bk,nb", [(1000, 32, 1), (700, 5, 3), (300, 64, 2)])
+def test_cached_prefix_key_split_tiny_f32(P, Pn, Bk, nb):
+    """Blocks over a long cached prefix with so few workgroups that the keys
+    are split over workgroups and their softmax states merged (8, 6 and 3
+    key ranges here; ragged block and prefix tiles), fp32 at 1e-4."""
+    from paper_2608_11742_amd._abi import KvCache
+    shape = synth.TINY
+    w_np = synth.model_weights_np(shape, seed=0, dtype="f32")
+    model = P.Model(shape, _upload(w_np, "f32"), dtype="f32", max_pos=Pn + Bk)
+    try:
+        prefix = synth.tokens_np(50 + Pn, "prefix", Pn, shape.vocab - 1)
+        k, vt, cap = model.new_kv_cache(Pn)
+        kvc = KvCache(k.data_ptr(), vt.data_ptr(), 0, cap)
+        model.forward(torch.from_numpy(prefix).to(DEV)[None], torch.arange(1, dtype=torch.int32, device=DEV),
+                      kv_out=kvc)
+        blocks = synth.tokens_np(51 + Bk, "blocks", nb * Bk, shape.vocab - 1).reshape(nb, Bk)
+        blocks[:, Bk // 2:] = shape.mask_id
+        lm = np.arange(Bk, dtype=np.int32)
+        kvc.len = Pn
+        out = model.forward(torch.from_numpy(blocks).to(DEV), torch.from_numpy(lm).to(DEV), pos_offset=Pn,
+                            kv_prefix=kvc, scale=4.0)
+        torch.cuda.synchronize()
+        kv = om.prefix_cache(prefix, w_np, shape)
+        refs = [om.lm_logits(om.hidden(blocks[b], w_np, shape, pos_offset=Pn, prefix_kv=kv), w_np, shape, scale=4.0)
+                for b in range(nb)]
+        ref = softmax_stats(np.concatenate(refs), 16)
+        print(compare_stats(out.numpy(), ref, 1e-4, label=f"key-split prefix {Pn} block {Bk} x {nb}"))
+    finally:
+        model.close()
+
+
+@pytest.mark.parametrize("Pn,Bk", [(20, 1), (20, 32), (100, 17), (130, 64), (64, 33), (448, 32)])
 def test_cached_prefix_forward_small_bf16(P, small_bf16, Pn, Bk):
     """Blocks of at most 64 queries over a cached bf16 prefix (the attention
     layout that splits a tile's keys between two waves and merges their
-    softmax states): a prefix shorter than half a key tile, ragged prefix
-    tiles, single-query blocks, against the mirror oracle."""
+    softmax states; at 130 + 64 and 448 + 32 keys also split over
+    workgroups): a prefix shorter than half a key tile, ragged prefix tiles,
+    single-query blocks, against the mirror oracle."""
     shape, w_np, model = small_bf16
     nb = 3
     prefix = synth.tokens_np(40 + Pn, "prefix", Pn, shape.vocab - 1)
