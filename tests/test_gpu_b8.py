@@ -181,7 +181,8 @@ def test_full_step_properties(P, b8_full):
 
 def test_cached_step_two_layer_8b_width(P, b8_two_layer):
     """KV-cached lookahead (1024 cached prefix positions, 16 branch blocks of 32):
-    branch 7 against the mirror oracle with the oracle's own prefix cache."""
+    branch 7 against the mirror oracle with the oracle's own prefix cache, in
+    the batch and alone (the batch-1 anchor forward's launches)."""
     from paper_2608_11742_amd._abi import KvCache
     shape, w, model = b8_two_layer
     Pn, Bk, nb = 1024, 32, 16
@@ -223,4 +224,13 @@ def test_cached_step_two_layer_8b_width(P, b8_two_layer):
     rep = compare_stats(got, ref, 2e-2, label="cached step 2-layer 8B width", logit_tol=logit_tol,
                         max_exceptions=max(2, 2 * own), id_ranks=4)
     print(f"oracle noise floor {spread:.3e}, logit bound {logit_tol:.3e}, oracle's own flips {own}", rep)
+    # the same block alone (batch 1, the step's anchor form): 32 workgroups of
+    # the 32-query attention layout, so each head's 17 key tiles are split
+    # over workgroups and merged, and the 32-row projections
+    out1 = model_p.forward(torch.from_numpy(blocks[b:b + 1]).to(DEV), torch.from_numpy(lm).to(DEV), pos_offset=Pn,
+                           kv_prefix=kv, scale=1.0)
+    torch.cuda.synchronize()
+    rep1 = compare_stats(out1.numpy(), ref, 2e-2, label="cached block alone 2-layer 8B width", logit_tol=logit_tol,
+                         max_exceptions=max(2, 2 * own), id_ranks=4)
+    print(rep1)
     model_p.close()
