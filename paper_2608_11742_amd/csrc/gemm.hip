@@ -376,27 +376,57 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
               *reinterpret_cast<const u32x4*>(st + off(r, c16));
         }
       } else {
-        // V^T (IEEE binary16, see pack_vt2): a lane's 4 values of a block are
-        // 4 consecutive positions of one head dim, i.e. 8 contiguous bytes of
-        // a V^T row: stored straight from registers (4 rows of one sequence
-        // when seq % 4 == 0)
-        uint16_t* vt = reinterpret_cast<uint16_t*>(o.vt);
-        const bool vec4 = (o.seq % 4) == 0 && (o.vt_ld % 4) == 0;
+        // V^T in IEEE binary16 (see pack_vt2).  A lane's 4 values of a block
+        // are 4 consecutive positions of one head dim (8 contiguous bytes of
+        // a V^T row).  A 64-row wave tile inside one sequence is staged
+        // transposed in the wave's own region of the idle ring, [dim][64
+        // positions] in rows of 8 chunks of 8 positions (chunk c of dim row d
+        // in slot c ^ (d % 8)), and written back with 16 bytes per lane, 8
+        // lanes per whole 128-byte V^T row; other tiles store the 8-byte
+        // pieces straight from registers.
+        bool staged = false;
+        if constexpr (TM::kWTM == 64) {
+          static_assert(TM::kWaves * 64 * 128 * 2 <= TM::kSmem, "v staging inside the ring");
+          if (o.seq % 64 == 0 && r0 + 64 <= M && o.vt_ld % 8 == 0) {
+            uint8_t* st = smem + wave * (64 * 128 * 2);
+            auto voff = [](int d, int p) { return d * 128 + (((p >> 3) ^ (d & 7)) << 4) + (p & 7) * 2; };
 #pragma unroll
-        for (int m = 0; m < TM::kFM; ++m) {
-          const int row = row_base + m * 16;   // rows row .. row + 3
-          if (row >= M) continue;
-          const int b = row / o.seq, sp = row - b * o.seq;
+            for (int m = 0; m < TM::kFM; ++m)
 #pragma unroll
-          for (int n = 0; n < TM::kFN; ++n) {
-            const int cin = cin0 + n * 16 + lc, h = cin / hd, dim = cin % hd;
-            if (vec4 && row + 3 < M) {
-              *reinterpret_cast<u32x2*>(vt + (size_t(b * o.H + h) * hd + dim) * o.vt_ld + sp) =
-                  u32x2{pack_vt2(acc[m][n][0], acc[m][n][1]), pack_vt2(acc[m][n][2], acc[m][n][3])};
-            } else {
-              for (int i = 0; i < 4 && row + i < M; ++i) {
-                const int bi = (row + i) / o.seq, si = (row + i) - bi * o.seq;
-                vt[(size_t(bi * o.H + h) * hd + dim) * o.vt_ld + si] = uint16_t(pack_vt2(acc[m][n][i], 0.f));
+              for (int n = 0; n < TM::kFN; ++n)
+                *reinterpret_cast<u32x2*>(st + voff(n * 16 + lc, m * 16 + 4 * (lane >> 4))) =
+                    u32x2{pack_vt2(acc[m][n][0], acc[m][n][1]), pack_vt2(acc[m][n][2], acc[m][n][3])};
+            const int b = r0 / o.seq, sp0 = r0 - b * o.seq;
+            uint16_t* vt = reinterpret_cast<uint16_t*>(o.vt);
+#pragma unroll
+            for (int it = 0; it < 128 * 8 / 64; ++it) {
+              const int q = lane + 64 * it, d = q >> 3, c = q & 7;
+              const int cin = cin0 + d, h = cin / hd, dim = cin % hd;
+              *reinterpret_cast<u32x4*>(vt + (size_t(b * o.H + h) * hd + dim) * o.vt_ld + sp0 + c * 8) =
+                  *reinterpret_cast<const u32x4*>(st + d * 128 + ((c ^ (d & 7)) << 4));
+            }
+            staged = true;
+          }
+        }
+        if (!staged) {
+          uint16_t* vt = reinterpret_cast<uint16_t*>(o.vt);
+          const bool vec4 = (o.seq % 4) == 0 && (o.vt_ld % 4) == 0;
+#pragma unroll
+          for (int m = 0; m < TM::kFM; ++m) {
+            const int row = row_base + m * 16;   // rows row .. row + 3
+            if (row >= M) continue;
+            const int b = row / o.seq, sp = row - b * o.seq;
+#pragma unroll
+            for (int n = 0; n < TM::kFN; ++n) {
+              const int cin = cin0 + n * 16 + lc, h = cin / hd, dim = cin % hd;
+              if (vec4 && row + 3 < M) {
+                *reinterpret_cast<u32x2*>(vt + (size_t(b * o.H + h) * hd + dim) * o.vt_ld + sp) =
+                    u32x2{pack_vt2(acc[m][n][0], acc[m][n][1]), pack_vt2(acc[m][n][2], acc[m][n][3])};
+              } else {
+                for (int i = 0; i < 4 && row + i < M; ++i) {
+                  const int bi = (row + i) / o.seq, si = (row + i) - bi * o.seq;
+                  vt[(size_t(bi * o.H + h) * hd + dim) * o.vt_ld + si] = uint16_t(pack_vt2(acc[m][n][i], 0.f));
+                }
               }
             }
           }
