@@ -77,6 +77,12 @@ int tile_rows(int kind, int M, int N, int K) {
   return M <= quad_max ? Quad::BM : Big::BM;
 }
 
+// Split-K parts of the QKV projection over 129-512 rows take 256 x 192 tiles:
+// 3 d / 192 column tiles by 1 or 2 row tiles, times the parts, fill the 256
+// CUs exactly for the 8B shape (128 x 2 or 64 x 4), where 256 x 256 tiles
+// leave a quarter of them idle (96 x 2 or 48 x 4)
+static bool qkv_mid_parts(int M, int N) { return M > 128 && M <= 512 && N % Mid::BN == 0; }
+
 // EPI_PART / EPI_PART_GU: split-K partial tiles (GU: the gate/up row pairing
 // of EPI_SWIGLU) written to part[split][M][np]
 enum { EPI_RESID = 0, EPI_SWIGLU = 1, EPI_QKV = 2, EPI_PART = 3, EPI_PART_GU = 4 };
@@ -231,9 +237,14 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
 
   if constexpr (kSplit) {
     // the fp32 partial tile through LDS as in the residual epilogue, 16-byte
-    // stores along rows of part[split]
-    static_assert((TM::kWTM % 64 == 0 || TM::kWTM == 32) && TM::kWTN == 128, "partial epilogue tiling");
-    constexpr int RG = TM::kWTM >= 64 ? 64 : TM::kWTM;   // rows per staged group
+    // stores along rows of part[split]: each wave stages RG rows by up to 64
+    // columns of its tile at a time (a 96-column wave tile as 64 + 32); RG is
+    // halved where the staging of all waves would not fit in the ring
+    static_assert((TM::kWTM % 64 == 0 || TM::kWTM == 32) &&
+                      (TM::kWTN == 128 || (TM::kWTN == 96 && EPI == EPI_PART)),
+                  "partial epilogue tiling");
+    constexpr int RG0 = TM::kWTM >= 64 ? 64 : TM::kWTM;
+    constexpr int RG = TM::kWaves * RG0 * 64 * 4 <= TM::kSmem ? RG0 : RG0 / 2;   // rows per staged group
     static_assert(TM::kWaves * RG * 64 * 4 <= TM::kSmem, "staging inside the ring");
     uint8_t* st = smem + wave * (RG * 64 * 4);
     auto slot_of = [](int r, int c4) { return r * 256 + (((c4 ^ (r & 15))) << 4); };
@@ -241,12 +252,14 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
 #pragma unroll
     for (int g = 0; g < TM::kWTM / RG; ++g) {   // row groups of the wave tile
       const int r0 = m0 + wm * TM::kWTM + RG * g;
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
+      static_for<0, cdiv(TM::kFN, 4)>([&](auto hh) {   // column groups of up to 64
+        constexpr int h = decltype(hh)::value;
+        constexpr int NB = TM::kFN - 4 * h < 4 ? TM::kFN - 4 * h : 4;   // 16-column blocks of the group
+        constexpr int CH = 4 * NB;                                      // 16-byte chunks of a staged row
 #pragma unroll
         for (int m = 0; m < RG / 16; ++m)
 #pragma unroll
-          for (int nn = 0; nn < 4; ++nn)
+          for (int nn = 0; nn < NB; ++nn)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const int r = m * 16 + 4 * (lane >> 4) + i, c = nn * 16 + lc;
@@ -254,14 +267,14 @@ __global__ __launch_bounds__(Cfg::kThreads, Cfg::kMinBlocks) void gemm_kernel(co
             }
         const int c0 = tn * Cfg::BN + wn * TM::kWTN + 64 * h;
 #pragma unroll
-        for (int j = 0; j < RG / 4; ++j) {
-          const int q = lane + 64 * j, r = q >> 4, c4 = q & 15;
+        for (int j = 0; j < RG * CH / 64; ++j) {
+          const int q = lane + 64 * j, r = q / CH, c4 = q % CH;
           const int row = r0 + r;
           if (row < M)
             *reinterpret_cast<f32x4*>(P + size_t(row) * ep.np + c0 + 4 * c4) =
                 *reinterpret_cast<const f32x4*>(st + slot_of(r, c4));
         }
-      }
+      });
     }
   } else if constexpr (EPI == EPI_RESID) {
     // x += acc through LDS: each wave stages half of its 64 x 128 tile at a
@@ -717,9 +730,11 @@ hipError_t splitk_add(const SplitK& sk, int M, int N, float* X, int ldx, hipStre
 }
 
 int gemm_splits(int kind, int M, int N, int K, int dtype) {
-  // workgroups that fill the 256 CUs: one Big or Quad workgroup per CU, two Small ones
+  // workgroups that fill the 256 CUs: one Big, Mid or Quad workgroup per CU, two Small ones
   const int bm = tile_rows(kind, M, N, K);
-  const int tiles_n = kind == GEMM_KIND_GATEUP ? cdiv(N / 2, 128) : cdiv(N, kBN);
+  const int tiles_n = kind == GEMM_KIND_GATEUP ? cdiv(N / 2, 128)
+                      : kind == GEMM_KIND_QKV && qkv_mid_parts(M, N) ? N / Mid::BN
+                                                                       : cdiv(N, kBN);
   const int tiles = cdiv(M, bm) * tiles_n, full = bm == Small::BM ? 512 : 256;
   const int stages = K / (dtype ? 64 : 32);   // 128-byte K stages
   if (tiles >= full * 5 / 8 || stages < 2) return 1;
@@ -813,8 +828,11 @@ hipError_t qkv_split(const void* A, int lda, const void* Wqkv, int M, int K, con
   ep.qkv = o;
   const int N = 3 * o.d, tn = cdiv(N, kBN);
   ep.part = sk.part;
-  ep.np = tn * kBN;
-  hipError_t e = launch<T, EPI_PART>(tile_rows(GEMM_KIND_QKV, M, N, K), A, lda, Wqkv, K, M, N, K, tn, ep, s, sk.splits);
+  ep.np = tn * kBN;   // the partial layout does not depend on the tiling
+  hipError_t e = qkv_mid_parts(M, N)
+                     ? launch_cfg<T, EPI_PART, 0, Mid>(A, lda, Wqkv, K, M, N, K, N / Mid::BN, ep, s, sk.splits)
+                     : launch<T, EPI_PART>(tile_rows(GEMM_KIND_QKV, M, N, K), A, lda, Wqkv, K, M, N, K, tn, ep, s,
+                                           sk.splits);
   if (e != hipSuccess) return e;
   const int n_qk = cdiv(M * (o.d / 4), kRedThreads), n_v = cdiv(o.d, 64) * cdiv(M, 16);
   if (o.hd == 128)
