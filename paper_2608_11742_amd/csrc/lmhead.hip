@@ -303,6 +303,8 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_kernel(const T* __restrict
         if (better(v, c0 + pos, tv[kK - 1], ti[kK - 1])) topk_insert(tv, ti, v, c0 + pos);
       }
     }
+    // the next pass prunes with the bound these insertions raised
+    if (pass + 1 < Cfg::kPasses) refresh_bound();
     __syncthreads();
     }
     if constexpr (!kListInMemory) refresh_bound();
