@@ -182,7 +182,8 @@ def test_full_step_properties(P, b8_full):
 def test_cached_step_two_layer_8b_width(P, b8_two_layer):
     """KV-cached lookahead (1024 cached prefix positions, 16 branch blocks of 32):
     branch 7 against the mirror oracle with the oracle's own prefix cache, in
-    the batch and alone (the batch-1 anchor forward's launches)."""
+    the batch, alone (the batch-1 anchor forward's launches) and in a ragged
+    batch of 10 blocks."""
     from paper_2608_11742_amd._abi import KvCache
     shape, w, model = b8_two_layer
     Pn, Bk, nb = 1024, 32, 16
@@ -233,4 +234,14 @@ def test_cached_step_two_layer_8b_width(P, b8_two_layer):
     rep1 = compare_stats(out1.numpy(), ref, 2e-2, label="cached block alone 2-layer 8B width", logit_tol=logit_tol,
                          max_exceptions=max(2, 2 * own), id_ranks=4)
     print(rep1)
+    # the same block in a ragged batch of 10 (320 rows per projection: QKV
+    # split-K parts on 256 x 192 tiles with a partial second row tile, O in 4
+    # and down in 8 K parts, gate/up on 256 x 192 tiles)
+    out10 = model_p.forward(torch.from_numpy(blocks[:10]).to(DEV), torch.from_numpy(lm).to(DEV), pos_offset=Pn,
+                            kv_prefix=kv, scale=1.0)
+    torch.cuda.synchronize()
+    got10 = {kk: v[b * Bk:(b + 1) * Bk] for kk, v in out10.numpy().items()}
+    rep10 = compare_stats(got10, ref, 2e-2, label="cached block in a batch of 10, 2-layer 8B width",
+                          logit_tol=logit_tol, max_exceptions=max(2, 2 * own), id_ranks=4)
+    print(rep10)
     model_p.close()
