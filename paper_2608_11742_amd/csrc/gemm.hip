@@ -3,7 +3,8 @@
 //   swiglu : f = silu(a Wg^T) * (a Wu^T)     (gate/up projection)
 //   qkv    : q, k, v = a Wqkv^T, rotary embedding on q and k, scattered to
 //            head-major Q/K and transposed V
-// 256x256 output tiles, 8 waves of 64x128, bf16 (or fp32) MFMA, fp32 accumulate.
+// 256x256 output tiles, 8 waves of 64x128, bf16 (or fp32) MFMA, fp32 accumulate;
+// fewer rows take the smaller tile configurations below.
 //
 // Few rows (a 512-row forward has 32 output tiles in the O and down
 // projections for 256 CUs): the K range is split into parts, every part
@@ -18,7 +19,7 @@ namespace dllm {
 
 namespace {
 
-// Tile configurations, both with waves of 64 x 128 (the epilogues' layout):
+// Tile configurations; Big and Small with waves of 64 x 128 (the epilogues' layout):
 // Big 256 x 256 with 8 waves (two per SIMD, one workgroup per CU); Small
 // 64 x 256 with 2 waves for GEMMs of at most kSmallM rows, where a 256-row
 // tile would mostly multiply clamped duplicate rows (two workgroups per CU).
@@ -40,7 +41,8 @@ using Small = GemmCfg<64, 256, 1, 2, 2>;
 using Quad = GemmCfg<128, 256, 4, 2, 1, true>;
 // gate/up with 257-512 rows: 256 x 192 tiles (waves of 64 x 96, 48 gate + 48
 // up rows each) give 2 x F / 96 = 256 workgroups for the 8B shape, one per CU,
-// where 256 x 256 tiles leave a quarter of the CUs idle
+// where 256 x 256 tiles leave a quarter of the CUs idle; also the split-K
+// parts of the QKV projection over 129-512 rows (qkv_mid_parts)
 using Mid = GemmCfg<256, 192, 4, 2, 2, true>;
 constexpr int kBN = 256;          // Big and Small: column tile of the split-K partials and the QKV / residual launches
 constexpr int kGroupM = 8;
